@@ -1,0 +1,221 @@
+"""Benchmark of the per-device HDP attention hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+A step is one causal attention forward + backward of the workload through the
+C ABI: device planning, forward, backward preprocess, backward, dQ finalize
+(and for the context-parallel workloads the per-step chunk calls plus the LSE
+merge).  Inputs are resident in HBM before timing starts; K steps are timed
+with HIP events on the library's stream, bracketed by device synchronisation.
+Prints ONE JSON line.
+
+FLOPs are causal-adjusted: forward 4*d*Hq*A, backward 10*d*Hq*A, where A is
+the exact number of visible (query, key) pairs.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+BF16_PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12   # 2516.6: MI355X dense bf16 MFMA (AMD's 2.5 PF)
+HBM_PEAK_GBS = 8000.0
+
+WORKLOADS = {
+    "packed7b": "7B-shaped packed varlen causal attention fwd+bwd: 32 q heads, 32 kv heads, "
+                "head_dim 128, one 32768-token buffer of log-normal lengths (median 1K, "
+                "clipped to [128, 32K]), seed 0",
+    "gqa70b": "70B-shaped GQA packed varlen causal attention fwd+bwd: 64 q heads, 8 kv heads, "
+              "head_dim 128, 131072 tokens, 1-2 long segments (32K-64K) + U[256,4K] shorts",
+    "cp7b": "context-parallel share on the 7B shape: a 32768-token Q chunk at offset 1015808 vs 8 "
+            "KV chunks of 32768 (7 past, 1 diagonal), fwd x8 + LSE merge + bwd x8",
+    "zigzag141b": "141B-shaped zig-zag CP share: 48 q heads, 8 kv heads, Q halves of 32768 at 0 "
+                  "and 229376 against the matching KV halves, fwd + merge + bwd",
+}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def visible_pairs_chunk(lq, lk, diag):
+    tot = 0
+    for i in range(lq):
+        tot += max(0, min(lk, i + diag + 1))
+    return tot
+
+
+def setup_varlen(name, seed, dev):
+    import torch
+    from paper_2502_21231_amd import inputs
+    if name == "packed7b":
+        lens, hq, hkv = inputs.lognormal_packed_lengths(seed), 32, 32
+    else:
+        lens, hq, hkv = inputs.mixed_long_short_lengths(seed), 64, 8
+    d, T = 128, sum(lens)
+    cu = torch.from_numpy(inputs.cu_seqlens(lens))
+    q = inputs.normal(seed, inputs.TID_Q, (T, hq, d))
+    k = inputs.normal(seed, inputs.TID_K, (T, hkv, d))
+    v = inputs.normal(seed, inputs.TID_V, (T, hkv, d))
+    do = inputs.normal(seed, inputs.TID_DO, (T, hq, d))
+    A = sum(l * (l + 1) // 2 for l in lens)
+    return dict(lens=lens, hq=hq, hkv=hkv, d=d, T=T, A=A, cu_cpu=cu, q_cpu=q, k_cpu=k, v_cpu=v,
+                do_cpu=do, cu=cu.to(dev), q=q.to(dev), k=k.to(dev), v=v.to(dev), do=do.to(dev))
+
+
+def run_varlen_bench(args, dev):
+    import torch
+    from paper_2502_21231_amd import bs_attn as B
+    W = setup_varlen(args.workload, args.seed, dev)
+    hq, hkv, d, T, A = W["hq"], W["hkv"], W["d"], W["T"], W["A"]
+    maxlen = max(W["lens"])
+    scale = 1.0 / math.sqrt(d)
+    dims = B.make_dims(W["q"], W["k"])
+    nseq = len(W["lens"])
+    ws_f = B.alloc_workspace(B.BS_OP_VARLEN_FWD, dims, dev, nseq, maxlen)
+    ws_b = B.alloc_workspace(B.BS_OP_VARLEN_BWD, dims, dev, nseq, maxlen)
+    out = torch.empty_like(W["q"])
+    lse = torch.empty(hq, T, dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(W["q"]), torch.empty_like(W["k"]), torch.empty_like(W["v"])
+
+    def step():
+        B.bs_attn_varlen_fwd(W["q"], W["k"], W["v"], W["cu"], W["cu"], maxlen, True, scale, out, lse, ws_f)
+        B.bs_attn_varlen_bwd(W["q"], W["k"], W["v"], out, lse, W["do"], W["cu"], W["cu"], maxlen, True,
+                             scale, dq, dk, dv, ws_b)
+
+    flops_fwd = 4 * d * hq * A
+    flops_bwd = 10 * d * hq * A
+    res = time_steps(step, args, dev, flops_fwd, flops_bwd)
+    B.bs_read_device_status(ws_b)
+    res["config"] = {"workload": WORKLOADS[args.workload], "tokens": T, "heads_q": hq, "heads_kv": hkv,
+                     "head_dim": d, "segments": nseq, "seed": args.seed, "visible_pairs": A,
+                     "longest_segment": maxlen}
+    res["flops_per_step"] = flops_fwd + flops_bwd
+    if args.cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_varlen(W, scale)
+    return res
+
+
+def time_steps(step, args, dev, flops_fwd, flops_bwd):
+    import torch
+    from paper_2502_21231_amd import bs_attn as B
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+    s = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    B.bs_set_profiling(True)
+    torch.cuda.synchronize(dev)
+    e0.record(s)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    e1.record(s)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+    total_ms = e0.elapsed_time(e1)
+    kern = {}
+    names = {B.BS_KERNEL_PLAN: "plan", B.BS_KERNEL_FWD: "fwd", B.BS_KERNEL_PREPROCESS: "bwd_preprocess",
+             B.BS_KERNEL_BWD: "bwd", B.BS_KERNEL_FINALIZE: "dq_finalize", B.BS_KERNEL_MERGE: "lse_merge"}
+    for kind, nm in names.items():
+        ms, n = B.bs_profile_read(kind)
+        if n:
+            kern[nm] = {"ms_per_step": ms / args.steps, "launches_per_step": n / args.steps,
+                        "avg_ms_per_launch": ms / n}
+    B.bs_set_profiling(False)
+    ms_step = total_ms / args.steps
+    flops = flops_fwd + flops_bwd
+    value = flops / (ms_step * 1e-3) / 1e12
+    fwd_ms = kern.get("fwd", {}).get("ms_per_step", float("nan"))
+    bwd_ms = kern.get("bwd", {}).get("ms_per_step", float("nan"))
+    dom = "bwd" if bwd_ms >= fwd_ms else "fwd"
+    dom_flops = flops_bwd if dom == "bwd" else flops_fwd
+    dom_launches = kern[dom]["launches_per_step"]
+    achieved = dom_flops / dom_launches / (kern[dom]["avg_ms_per_launch"] * 1e-3) / 1e12
+    return {
+        "value": value, "ms_per_step": ms_step, "wall_s": wall,
+        "pct_of_bf16_peak": 100.0 * value / BF16_PEAK_TFLOPS,
+        "fwd_tflops": flops_fwd / (fwd_ms * 1e-3) / 1e12 if fwd_ms == fwd_ms else None,
+        "bwd_tflops": flops_bwd / (bwd_ms * 1e-3) / 1e12 if bwd_ms == bwd_ms else None,
+        "kernels": kern,
+        "roofline": {"kernel": f"bs_attn {dom} (bf16 MFMA)", "bound": "mfma", "achieved": achieved,
+                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": achieved / BF16_PEAK_TFLOPS,
+                     "traffic": None},
+    }
+
+
+def cpu_baseline_varlen(W, scale):
+    """The float64 oracle on one query head of the same workload (fwd + bwd, all segments)."""
+    import numpy as np
+    import torch
+    from oracle import attention as A
+    try:
+        import threadpoolctl
+        cores = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()
+                    if i.get("user_api") == "blas")
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    hq, hkv, d = W["hq"], W["hkv"], W["d"]
+    g = hq // hkv
+    q = W["q_cpu"][:, :1]
+    k = W["k_cpu"][:, :1]
+    v = W["v_cpu"][:, :1]
+    do = W["do_cpu"][:, :1]
+    cu = W["cu_cpu"].numpy()
+    t0 = time.perf_counter()
+    o, l = A.varlen_fwd(q, k, v, cu, cu, True, scale)
+    A.varlen_bwd(q, k, v, o, l, do, cu, cu, True, scale)
+    dt = time.perf_counter() - t0
+    flops = 14 * d * 1 * W["A"]
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"query head 0 of {hq} (KV head 0, group of {g}), all {len(W['lens'])} segments, "
+                      f"fwd+bwd in float64 NumPy: {flops:.3e} FLOP in {dt:.1f} s",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="packed7b")
+    ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU's share of the work; --gpus {args.gpus} is not supported "
+              f"(this build has no multi-GPU path: use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    if args.workload in ("packed7b", "gqa70b"):
+        res = run_varlen_bench(args, dev)
+    else:
+        raise SystemExit(f"workload {args.workload} is not implemented yet")
+    line = {
+        "metric": "attention fwd+bwd TFLOP/s (causal-adjusted) and % of bf16 MFMA peak, 1 GPU",
+        "value": round(res["value"], 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(res["ms_per_step"], 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": res["config"],
+        "pct_of_bf16_peak": round(res["pct_of_bf16_peak"], 2),
+        "fwd_tflops": res["fwd_tflops"], "bwd_tflops": res["bwd_tflops"],
+        "kernels": res["kernels"], "flops_per_step": res["flops_per_step"],
+        "roofline": res["roofline"],
+        "cpu_baseline": res.get("cpu_baseline"),
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

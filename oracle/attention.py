@@ -47,14 +47,16 @@ def _as64(x) -> np.ndarray:
     return np.asarray(x, dtype=np.float64)
 
 
-def visible_mask(len_q: int, len_k: int, diag, causal: bool) -> np.ndarray:
-    """Boolean [len_q, len_k]: key j is visible to query i iff j - i <= diag.
+def visible_mask(len_q: int, len_k: int, diag, causal: bool, rows=None) -> np.ndarray:
+    """Boolean [len_q, len_k] (or [r1 - r0, len_k] for rows = (r0, r1)): key j is visible
+    to query i iff j - i <= diag.
 
     `diag` is len_k - len_q for a varlen segment (bottom-right alignment) and
     q_off - k_off for a context-parallel chunk; non-causal sees every key."""
+    r0, r1 = (0, len_q) if rows is None else rows
     if not causal:
-        return np.ones((len_q, len_k), dtype=bool)
-    i = np.arange(len_q, dtype=np.int64)[:, None]
+        return np.ones((r1 - r0, len_k), dtype=bool)
+    i = np.arange(r0, r1, dtype=np.int64)[:, None]
     j = np.arange(len_k, dtype=np.int64)[None, :]
     return (j - i) <= int(diag)
 
@@ -88,7 +90,7 @@ def _segment_fwd(q, k, v, scale, diag, causal, hq, hkv):
         kh, vh = k[:, h // g, :], v[:, h // g, :]
         for r0 in range(0, lq, ROW_BLOCK):
             r1 = min(lq, r0 + ROW_BLOCK)
-            mask = visible_mask(lq, lk, diag, causal)[r0:r1]
+            mask = visible_mask(lq, lk, diag, causal, (r0, r1))
             if lk == 0:
                 continue
             o[r0:r1, h, :], lse[h, r0:r1] = _attend_rows(q[r0:r1, h, :], kh, vh, mask, scale)
@@ -158,7 +160,7 @@ def _segment_bwd(q, k, v, o, lse, do, scale, diag, causal, hq, hkv):
         kh, vh = k[:, kv, :], v[:, kv, :]
         for r0 in range(0, lq, ROW_BLOCK):
             r1 = min(lq, r0 + ROW_BLOCK)
-            mask = visible_mask(lq, lk, diag, causal)[r0:r1]
+            mask = visible_mask(lq, lk, diag, causal, (r0, r1))
             qb, dob, ob, lb = q[r0:r1, h, :], do[r0:r1, h, :], o[r0:r1, h, :], lse[h, r0:r1]
             s = scale * (qb @ kh.T)
             ok = mask & np.isfinite(lb)[:, None]

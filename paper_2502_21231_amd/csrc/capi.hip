@@ -1,0 +1,496 @@
+// C ABI of libbs_attn.so: argument validation, workspace layout, launch order.
+// The declarations and the contract of every entry point are in bs_attn.h.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <atomic>
+#include <mutex>
+#include <vector>
+
+#include "common.hpp"
+
+namespace bs {
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return BS_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(BS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int64_t kMaxTokens = int64_t(1) << 30;
+
+// Profiling: pairs of HIP events recorded around each kernel launch while enabled.
+struct Profiler {
+  std::mutex mu;
+  std::atomic<bool> on{false};
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> recs[BS_KERNEL_COUNT];
+  std::vector<hipEvent_t> spare;
+};
+
+Profiler& prof() {
+  static Profiler* p = new Profiler();  // never destroyed: events may outlive static teardown
+  return *p;
+}
+
+hipEvent_t take_event() {
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> g(P.mu);
+  if (!P.spare.empty()) {
+    hipEvent_t e = P.spare.back();
+    P.spare.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Records an event pair around the launches made during its lifetime.
+class ProfScope {
+ public:
+  ProfScope(int kind, hipStream_t s) : kind_(kind), s_(s) {
+    if (!prof().on.load(std::memory_order_relaxed)) return;
+    a_ = take_event();
+    b_ = take_event();
+    if (a_ && b_) hipEventRecord(a_, s_);
+  }
+  ~ProfScope() {
+    if (!a_ || !b_) return;
+    hipEventRecord(b_, s_);
+    Profiler& P = prof();
+    std::lock_guard<std::mutex> g(P.mu);
+    P.recs[kind_].emplace_back(a_, b_);
+  }
+
+ private:
+  int kind_;
+  hipStream_t s_;
+  hipEvent_t a_ = nullptr, b_ = nullptr;
+};
+
+struct PlanCfg {
+  PlanKind kind;
+  int tile_a, tile_b;
+};
+
+bool is_bwd(int op) { return op == BS_OP_VARLEN_BWD || op == BS_OP_CHUNK_BWD; }
+bool is_varlen(int op) { return op == BS_OP_VARLEN_FWD || op == BS_OP_VARLEN_BWD; }
+
+// Plans an op runs, in launch order (float32 backward plans twice: query tiles
+// for dQ, then key tiles for dK/dV).
+int plans_of(int op, int dtype, PlanCfg out[2]) {
+  if (dtype == BS_BF16) {
+    out[0] = is_bwd(op) ? PlanCfg{kPlanBwd, kBwdBN, kBwdBM} : PlanCfg{kPlanFwd, kFwdBM, kFwdBN};
+    return 1;
+  }
+  out[0] = PlanCfg{kPlanFwd, kF32BM, kF32BN};
+  if (!is_bwd(op)) return 1;
+  out[1] = PlanCfg{kPlanBwd, kF32BN, kF32BM};
+  return 2;
+}
+
+int64_t max_items_of(const PlanCfg& c, const bs_dims& d, int64_t nseg, bool varlen) {
+  const int64_t ta = c.kind == kPlanFwd ? d.total_q : d.total_k;
+  return (ta + c.tile_a - 1) / c.tile_a + (varlen ? nseg : 0);
+}
+
+int check_dims(const bs_dims* d, bool need_kv) {
+  if (d == nullptr) return fail(BS_ERR_INVALID_ARG, "dims is NULL");
+  if (d->dtype != BS_F32 && d->dtype != BS_BF16)
+    return fail(BS_ERR_UNSUPPORTED, "dtype %d is not BS_F32 or BS_BF16", d->dtype);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(BS_ERR_UNSUPPORTED, "head_dim %d is not 64 or 128", d->head_dim);
+  if (d->hq < 1) return fail(BS_ERR_INVALID_ARG, "hq = %d must be >= 1", d->hq);
+  if (d->total_q < 0 || d->total_q >= kMaxTokens)
+    return fail(BS_ERR_INVALID_ARG, "total_q = %lld out of [0, 2^30)", (long long)d->total_q);
+  if (need_kv) {
+    if (d->hkv < 1 || d->hq % d->hkv != 0)
+      return fail(BS_ERR_INVALID_ARG, "hq = %d must be a positive multiple of hkv = %d", d->hq, d->hkv);
+    if (d->total_k < 0 || d->total_k >= kMaxTokens)
+      return fail(BS_ERR_INVALID_ARG, "total_k = %lld out of [0, 2^30)", (long long)d->total_k);
+  }
+  return BS_OK;
+}
+
+int check_ptr(const void* p, int64_t count, const char* name) {
+  if (count == 0) return BS_OK;
+  if (p == nullptr) return fail(BS_ERR_INVALID_ARG, "%s is NULL", name);
+  if (reinterpret_cast<uintptr_t>(p) % 16 != 0)
+    return fail(BS_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return BS_OK;
+}
+
+int check_scale(float s) {
+  if (!isfinite(s) || !(s > 0.f)) return fail(BS_ERR_INVALID_ARG, "scale must be finite and > 0");
+  return BS_OK;
+}
+
+WsLayout layout_of(int op, const bs_dims& d, int64_t nseg) {
+  WsLayout L = {};
+  PlanCfg cfg[2];
+  const int np = plans_of(op, d.dtype, cfg);
+  const bool varlen = is_varlen(op);
+  int64_t mi = 0;
+  for (int i = 0; i < np; ++i) {
+    const int64_t m = max_items_of(cfg[i], d, nseg, varlen);
+    mi = m > mi ? m : mi;
+  }
+  size_t off = align256(sizeof(WsHeader));
+  L.seg_off = off;
+  off += align256(sizeof(int32_t) * (size_t)(nseg + 2));
+  L.unsorted = off;
+  off += align256(sizeof(WorkItem) * (size_t)mi);
+  L.sorted = off;
+  off += align256(sizeof(WorkItem) * (size_t)mi);
+  if (is_bwd(op)) {
+    L.dvec = off;
+    off += align256(sizeof(float) * (size_t)(d.hq * d.total_q));
+    if (varlen) {
+      L.dq_acc = off;
+      off += align256(sizeof(float) * (size_t)(d.total_q * d.hq * d.head_dim));
+    }
+  }
+  L.total = off;
+  L.max_items = mi;
+  return L;
+}
+
+int check_ws(const WsLayout& L, const void* ws, size_t bytes) {
+  if (ws == nullptr) return fail(BS_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+    return fail(BS_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (bytes < L.total)
+    return fail(BS_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", bytes,
+                L.total);
+  return BS_OK;
+}
+
+// Runs plan `i` of the op; returns the layout with max_items set for that plan.
+hipError_t run_plan(int op, const bs_dims& d, int i, const int32_t* cu_q, const int32_t* cu_k,
+                    int32_t num_seqs, int32_t max_seqlen, int64_t q_off, int64_t k_off,
+                    int causal, void* ws, const WsLayout& L, WsLayout* Lp, hipStream_t s) {
+  PlanCfg cfg[2];
+  plans_of(op, d.dtype, cfg);
+  const bool varlen = is_varlen(op);
+  *Lp = L;
+  Lp->max_items = max_items_of(cfg[i], d, varlen ? num_seqs : 1, varlen);
+  int64_t diag = q_off - k_off;
+  diag = diag < -kDiagClamp ? -kDiagClamp : (diag > kDiagClamp ? kDiagClamp : diag);
+  return launch_plan(cfg[i].kind, varlen ? cu_q : nullptr, varlen ? cu_k : nullptr,
+                     varlen ? num_seqs : 1, d.total_q, d.total_k, max_seqlen, (int32_t)diag,
+                     causal, cfg[i].tile_a, cfg[i].tile_b, Lp->max_items, ws, *Lp, s);
+}
+
+int check_varlen_args(const int32_t* cu_q, const int32_t* cu_k, int32_t num_seqs, int32_t max_seqlen) {
+  if (num_seqs < 0) return fail(BS_ERR_INVALID_ARG, "num_seqs = %d < 0", num_seqs);
+  if (max_seqlen < 0) return fail(BS_ERR_INVALID_ARG, "max_seqlen = %d < 0", max_seqlen);
+  if (cu_q == nullptr || cu_k == nullptr) return fail(BS_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  return BS_OK;
+}
+
+#define BS_TRY(x)                 \
+  do {                            \
+    int rc__ = (x);               \
+    if (rc__ != BS_OK) return rc__; \
+  } while (0)
+#define BS_HIP(x, what)                        \
+  do {                                         \
+    hipError_t e__ = (x);                      \
+    if (e__ != hipSuccess) return hip_fail(e__, what); \
+  } while (0)
+
+int fwd_common(int op, const bs_dims* dims, const void* q, const void* k, const void* v,
+               const int32_t* cu_q, const int32_t* cu_k, int32_t num_seqs, int32_t max_seqlen,
+               int64_t q_off, int64_t k_off, int causal, float scale, void* out, float* lse,
+               void* ws, size_t ws_bytes, void* stream) {
+  BS_TRY(check_dims(dims, true));
+  const bs_dims& d = *dims;
+  const int64_t qn = d.total_q * d.hq * d.head_dim, kn = d.total_k * d.hkv * d.head_dim;
+  BS_TRY(check_ptr(q, qn, "q"));
+  BS_TRY(check_ptr(k, kn, "k"));
+  BS_TRY(check_ptr(v, kn, "v"));
+  BS_TRY(check_ptr(out, qn, "out"));
+  BS_TRY(check_ptr(lse, d.total_q * d.hq, "lse"));
+  BS_TRY(check_scale(scale));
+  if (is_varlen(op)) BS_TRY(check_varlen_args(cu_q, cu_k, num_seqs, max_seqlen));
+  const WsLayout L = layout_of(op, d, is_varlen(op) ? num_seqs : 1);
+  BS_TRY(check_ws(L, ws, ws_bytes));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  WsLayout Lp;
+  {
+    ProfScope ps(BS_KERNEL_PLAN, s);
+    BS_HIP(run_plan(op, d, 0, cu_q, cu_k, num_seqs, max_seqlen, q_off, k_off, causal, ws, L, &Lp, s),
+           "planner launch");
+  }
+  ProfScope ps(BS_KERNEL_FWD, s);
+  if (d.dtype == BS_BF16)
+    BS_HIP(launch_fwd_bf16(d, q, k, v, causal, scale, out, lse, ws, Lp, s), "forward launch");
+  else
+    BS_HIP(launch_fwd_f32(d, q, k, v, causal, scale, out, lse, ws, Lp, s), "forward launch");
+  return ok();
+}
+
+int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const void* v,
+               const void* out, const float* lse, const void* dout, const int32_t* cu_q,
+               const int32_t* cu_k, int32_t num_seqs, int32_t max_seqlen, int64_t q_off,
+               int64_t k_off, int causal, float scale, float* dq_accum, void* dq, void* dk,
+               void* dv, void* ws, size_t ws_bytes, void* stream) {
+  BS_TRY(check_dims(dims, true));
+  const bs_dims& d = *dims;
+  const int64_t qn = d.total_q * d.hq * d.head_dim, kn = d.total_k * d.hkv * d.head_dim;
+  BS_TRY(check_ptr(q, qn, "q"));
+  BS_TRY(check_ptr(k, kn, "k"));
+  BS_TRY(check_ptr(v, kn, "v"));
+  BS_TRY(check_ptr(out, qn, "out"));
+  BS_TRY(check_ptr(lse, d.total_q * d.hq, "lse"));
+  BS_TRY(check_ptr(dout, qn, "dout"));
+  BS_TRY(check_ptr(dk, kn, "dk"));
+  BS_TRY(check_ptr(dv, kn, "dv"));
+  const bool varlen = is_varlen(op);
+  if (varlen) BS_TRY(check_ptr(dq, qn, "dq"));
+  else BS_TRY(check_ptr(dq_accum, qn, "dq_accum"));
+  BS_TRY(check_scale(scale));
+  if (varlen) BS_TRY(check_varlen_args(cu_q, cu_k, num_seqs, max_seqlen));
+  const WsLayout L = layout_of(op, d, varlen ? num_seqs : 1);
+  BS_TRY(check_ws(L, ws, ws_bytes));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* base = static_cast<char*>(ws);
+  float* dvec = reinterpret_cast<float*>(base + L.dvec);
+  float* acc = varlen ? reinterpret_cast<float*>(base + L.dq_acc) : dq_accum;
+  WsLayout Lp;
+  {
+    ProfScope ps(BS_KERNEL_PLAN, s);
+    BS_HIP(run_plan(op, d, 0, cu_q, cu_k, num_seqs, max_seqlen, q_off, k_off, causal, ws, L, &Lp, s),
+           "planner launch");
+  }
+  {
+    ProfScope ps(BS_KERNEL_PREPROCESS, s);
+    BS_HIP(launch_bwd_preprocess(d, out, dout, dvec, varlen ? acc : nullptr, ws, s),
+           "preprocess launch");
+  }
+  if (d.dtype == BS_BF16) {
+    ProfScope ps(BS_KERNEL_BWD, s);
+    BS_HIP(launch_bwd_bf16(d, q, k, v, dout, lse, dvec, acc, causal, scale, dk, dv, ws, Lp, s),
+           "backward launch");
+  } else {
+    {
+      ProfScope ps(BS_KERNEL_BWD, s);
+      BS_HIP(launch_bwd_f32_dq(d, q, k, v, lse, dout, dvec, causal, scale, acc, ws, Lp, s),
+             "backward dQ launch");
+    }
+    {
+      ProfScope ps(BS_KERNEL_PLAN, s);
+      BS_HIP(run_plan(op, d, 1, cu_q, cu_k, num_seqs, max_seqlen, q_off, k_off, causal, ws, L, &Lp, s),
+             "planner launch");
+    }
+    ProfScope ps(BS_KERNEL_BWD, s);
+    BS_HIP(launch_bwd_f32_dkdv(d, q, k, v, lse, dout, dvec, causal, scale, dk, dv, ws, Lp, s),
+           "backward dK/dV launch");
+  }
+  if (varlen) {
+    ProfScope ps(BS_KERNEL_FINALIZE, s);
+    BS_HIP(launch_dq_finalize(d, acc, dq, ws, s), "dQ finalize launch");
+  }
+  return ok();
+}
+
+}  // namespace
+}  // namespace bs
+
+using namespace bs;
+
+extern "C" {
+
+size_t bs_attn_workspace_size(int op, const bs_dims* dims, int32_t num_seqs, int32_t max_seqlen) {
+  if (op < BS_OP_VARLEN_FWD || op > BS_OP_CHUNK_BWD) {
+    fail(BS_ERR_UNSUPPORTED, "unknown op %d", op);
+    return 0;
+  }
+  if (check_dims(dims, true) != BS_OK) return 0;
+  if (is_varlen(op) && (num_seqs < 0 || max_seqlen < 0)) {
+    fail(BS_ERR_INVALID_ARG, "num_seqs and max_seqlen must be >= 0");
+    return 0;
+  }
+  ok();
+  return layout_of(op, *dims, is_varlen(op) ? num_seqs : 1).total;
+}
+
+int bs_attn_varlen_fwd(const bs_dims* dims, const void* q, const void* k, const void* v,
+                       const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k, int32_t num_seqs,
+                       int32_t max_seqlen, int causal, float scale, void* out, float* lse,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  return fwd_common(BS_OP_VARLEN_FWD, dims, q, k, v, cu_seqlens_q, cu_seqlens_k, num_seqs,
+                    max_seqlen, 0, 0, causal, scale, out, lse, workspace, workspace_bytes, stream);
+}
+
+int bs_attn_varlen_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,
+                       const void* out, const float* lse, const void* dout,
+                       const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k, int32_t num_seqs,
+                       int32_t max_seqlen, int causal, float scale, void* dq, void* dk, void* dv,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  return bwd_common(BS_OP_VARLEN_BWD, dims, q, k, v, out, lse, dout, cu_seqlens_q, cu_seqlens_k,
+                    num_seqs, max_seqlen, 0, 0, causal, scale, nullptr, dq, dk, dv, workspace,
+                    workspace_bytes, stream);
+}
+
+int bs_attn_chunk_fwd(const bs_dims* dims, const void* q, const void* k, const void* v,
+                      int64_t q_pos_offset, int64_t k_pos_offset, int causal, float scale,
+                      void* out, float* lse, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  return fwd_common(BS_OP_CHUNK_FWD, dims, q, k, v, nullptr, nullptr, 1, 0, q_pos_offset,
+                    k_pos_offset, causal, scale, out, lse, workspace, workspace_bytes, stream);
+}
+
+int bs_attn_chunk_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,
+                      const void* out_merged, const float* lse_merged, const void* dout,
+                      int64_t q_pos_offset, int64_t k_pos_offset, int causal, float scale,
+                      float* dq_accum, void* dk, void* dv, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  return bwd_common(BS_OP_CHUNK_BWD, dims, q, k, v, out_merged, lse_merged, dout, nullptr, nullptr,
+                    1, 0, q_pos_offset, k_pos_offset, causal, scale, dq_accum, nullptr, dk, dv,
+                    workspace, workspace_bytes, stream);
+}
+
+int bs_dq_finalize(const bs_dims* dims, const float* dq_accum, void* dq, void* stream) {
+  BS_TRY(check_dims(dims, false));
+  const int64_t qn = dims->total_q * dims->hq * dims->head_dim;
+  BS_TRY(check_ptr(dq_accum, qn, "dq_accum"));
+  BS_TRY(check_ptr(dq, qn, "dq"));
+  ProfScope ps(BS_KERNEL_FINALIZE, static_cast<hipStream_t>(stream));
+  BS_HIP(launch_dq_finalize(*dims, dq_accum, dq, nullptr, static_cast<hipStream_t>(stream)),
+         "dQ finalize launch");
+  return ok();
+}
+
+int bs_lse_merge(const bs_dims* dims, const void* out_partials, const float* lse_partials,
+                 int32_t n, void* out, float* lse, void* stream) {
+  BS_TRY(check_dims(dims, false));
+  if (n < 1) return fail(BS_ERR_INVALID_ARG, "n = %d must be >= 1", n);
+  const int64_t qn = dims->total_q * dims->hq * dims->head_dim;
+  BS_TRY(check_ptr(out_partials, qn * n, "out_partials"));
+  BS_TRY(check_ptr(lse_partials, dims->total_q * dims->hq * n, "lse_partials"));
+  BS_TRY(check_ptr(out, qn, "out"));
+  BS_TRY(check_ptr(lse, dims->total_q * dims->hq, "lse"));
+  ProfScope ps(BS_KERNEL_MERGE, static_cast<hipStream_t>(stream));
+  BS_HIP(launch_lse_merge(*dims, out_partials, lse_partials, n, out, lse,
+                          static_cast<hipStream_t>(stream)),
+         "merge launch");
+  return ok();
+}
+
+int bs_read_device_status(const void* workspace, void* stream) {
+  if (workspace == nullptr) return fail(BS_ERR_WORKSPACE, "workspace is NULL");
+  WsHeader h;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  BS_HIP(hipMemcpyAsync(&h, workspace, sizeof(h), hipMemcpyDeviceToHost, s), "status copy");
+  BS_HIP(hipStreamSynchronize(s), "status sync");
+  if (h.status != BS_DEV_OK)
+    return fail(BS_ERR_DEVICE_STATUS, "device planner rejected cu_seqlens: code %d", h.status);
+  return ok();
+}
+
+int bs_attn_plan_export(int op, const bs_dims* dims, const int32_t* cu_seqlens_q,
+                        const int32_t* cu_seqlens_k, int32_t num_seqs, int32_t max_seqlen,
+                        int64_t q_pos_offset, int64_t k_pos_offset, int causal, void* workspace,
+                        size_t workspace_bytes, int32_t* host_items, size_t capacity,
+                        size_t* count, int32_t* tile_m, int32_t* tile_n, void* stream) {
+  if (op < BS_OP_VARLEN_FWD || op > BS_OP_CHUNK_BWD) return fail(BS_ERR_UNSUPPORTED, "unknown op %d", op);
+  BS_TRY(check_dims(dims, true));
+  if (count == nullptr || (capacity > 0 && host_items == nullptr))
+    return fail(BS_ERR_INVALID_ARG, "count / host_items is NULL");
+  const bool varlen = is_varlen(op);
+  if (varlen) BS_TRY(check_varlen_args(cu_seqlens_q, cu_seqlens_k, num_seqs, max_seqlen));
+  const WsLayout L = layout_of(op, *dims, varlen ? num_seqs : 1);
+  BS_TRY(check_ws(L, workspace, workspace_bytes));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // the plan the op's main kernel walks: the last one of the op
+  PlanCfg cfg[2];
+  const int np = plans_of(op, dims->dtype, cfg);
+  WsLayout Lp;
+  BS_HIP(run_plan(op, *dims, np - 1, cu_seqlens_q, cu_seqlens_k, num_seqs, max_seqlen,
+                  q_pos_offset, k_pos_offset, causal, workspace, L, &Lp, s),
+         "planner launch");
+  WsHeader h;
+  BS_HIP(hipMemcpyAsync(&h, workspace, sizeof(h), hipMemcpyDeviceToHost, s), "plan copy");
+  BS_HIP(hipStreamSynchronize(s), "plan sync");
+  if (h.status != BS_DEV_OK)
+    return fail(BS_ERR_DEVICE_STATUS, "device planner rejected cu_seqlens: code %d", h.status);
+  const size_t n = (size_t)h.n_items;
+  *count = n;
+  if (tile_m) *tile_m = cfg[np - 1].kind == kPlanFwd ? cfg[np - 1].tile_a : cfg[np - 1].tile_b;
+  if (tile_n) *tile_n = cfg[np - 1].kind == kPlanFwd ? cfg[np - 1].tile_b : cfg[np - 1].tile_a;
+  const size_t m = n < capacity ? n : capacity;
+  if (m > 0) {
+    std::vector<WorkItem> items(m);
+    BS_HIP(hipMemcpyAsync(items.data(), static_cast<char*>(workspace) + L.sorted,
+                          m * sizeof(WorkItem), hipMemcpyDeviceToHost, s),
+           "plan copy");
+    BS_HIP(hipStreamSynchronize(s), "plan sync");
+    for (size_t i = 0; i < m; ++i) {
+      const WorkItem& w = items[i];
+      int32_t* o = host_items + 12 * i;
+      const int32_t common[6] = {w.seg, w.tile, w.a_start, w.a_rows, w.b_start, w.b_len};
+      memcpy(o, common, sizeof(common));
+      if (cfg[np - 1].kind == kPlanFwd) {
+        o[6] = w.n0; o[7] = w.n1; o[8] = w.diag; o[9] = 0;
+      } else {
+        o[6] = w.n0; o[7] = w.n1; o[8] = w.n2; o[9] = w.diag;
+      }
+      o[10] = 0;
+      o[11] = 0;
+    }
+  }
+  return ok();
+}
+
+int bs_set_profiling(int enable) {
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> g(P.mu);
+  for (auto& v : P.recs) {
+    for (auto& pr : v) {
+      hipEventSynchronize(pr.second);
+      P.spare.push_back(pr.first);
+      P.spare.push_back(pr.second);
+    }
+    v.clear();
+  }
+  P.on.store(enable != 0);
+  return ok();
+}
+
+int bs_profile_read(int kind, double* total_ms, int64_t* launches) {
+  if (kind < 0 || kind >= BS_KERNEL_COUNT) return fail(BS_ERR_INVALID_ARG, "unknown kernel kind %d", kind);
+  if (total_ms == nullptr || launches == nullptr) return fail(BS_ERR_INVALID_ARG, "NULL output");
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> g(P.mu);
+  double sum = 0.0;
+  for (auto& pr : P.recs[kind]) {
+    BS_HIP(hipEventSynchronize(pr.second), "event sync");
+    float ms = 0.f;
+    BS_HIP(hipEventElapsedTime(&ms, pr.first, pr.second), "event elapsed");
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = (int64_t)P.recs[kind].size();
+  return ok();
+}
+
+const char* bs_last_error(void) { return g_err; }
+
+}  // extern "C"

@@ -1,0 +1,227 @@
+// Device work planner: cu_seqlens (or chunk offsets) -> ordered list of tiles.
+//
+// The paper observes that the work of a packed micro-batch is proportional to
+// the area of its attention mask, not to its token count (Sec. 3.3, Imbalanced
+// FLOPs; Sec. 7, Dist-attn with packing).  The planner enumerates, per segment,
+// the query tiles (forward) or key tiles (backward), counts the tiles of the
+// other side that carry visible pairs, separates the FULL ones (no score mask
+// needed) from the MASKED ones (causal diagonal or ragged key tail), and orders
+// the list by descending cost so that a grid walking it in block order starts
+// the longest tiles first (longest-processing-time-first balancing of the
+// long-tailed length mix).  Tiles with no visible pair are never listed.
+//
+// Three kernels, all on the caller's stream and without host synchronisation:
+//   plan_count : validate cu_seqlens, per-segment tile counts, exclusive scan
+//   plan_emit  : one thread per list entry, fills its fields
+//   plan_sort  : stable rank by (cost desc, list index asc) and scatter
+#include "common.hpp"
+
+namespace bs {
+namespace {
+
+constexpr int kCountThreads = 1024;
+
+__device__ __forceinline__ void set_status(int32_t* st, int code) {
+  atomicCAS(st, 0, code);  // keeps the first error seen
+}
+
+// Segment b of the problem: query start/length, key start/length, diagonal.
+struct Seg {
+  int64_t q0, lq, k0, lk;
+  int32_t diag;
+};
+
+__device__ __forceinline__ int32_t clamp_diag(int64_t d) {
+  return (int32_t)(d < -kDiagClamp ? -kDiagClamp : (d > kDiagClamp ? kDiagClamp : d));
+}
+
+__device__ __forceinline__ Seg load_seg(const int32_t* cu_q, const int32_t* cu_k, int32_t b,
+                                        int64_t total_q, int64_t total_k, int32_t diag_chunk) {
+  Seg s;
+  if (cu_q == nullptr) {  // chunk mode: one segment, diagonal from the offsets
+    s.q0 = 0; s.lq = total_q; s.k0 = 0; s.lk = total_k; s.diag = diag_chunk;
+  } else {
+    s.q0 = cu_q[b]; s.lq = (int64_t)cu_q[b + 1] - cu_q[b];
+    s.k0 = cu_k[b]; s.lk = (int64_t)cu_k[b + 1] - cu_k[b];
+    s.diag = clamp_diag(s.lk - s.lq);
+  }
+  return s;
+}
+
+// Validates cu_seqlens, computes items per segment and their exclusive prefix.
+__global__ __launch_bounds__(kCountThreads) void plan_count(
+    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int32_t num_seqs,
+    int64_t total_q, int64_t total_k, int32_t max_seqlen, int kind, int tile_a,
+    WsHeader* __restrict__ hdr, int32_t* __restrict__ seg_off) {
+  __shared__ int32_t scan[kCountThreads];
+  __shared__ int32_t carry;
+  __shared__ int32_t status;
+  const int t = threadIdx.x;
+  if (t == 0) { carry = 0; status = 0; }
+  __syncthreads();
+  const int32_t nseg = cu_q == nullptr ? 1 : num_seqs;
+  if (cu_q != nullptr && t == 0) {
+    if (cu_q[0] != 0 || cu_k[0] != 0) set_status(&status, BS_DEV_BAD_FIRST);
+    if (cu_q[num_seqs] != total_q || cu_k[num_seqs] != total_k) set_status(&status, BS_DEV_BAD_TOTAL);
+  }
+  for (int32_t base = 0; base < nseg; base += kCountThreads) {
+    const int32_t b = base + t;
+    int32_t cnt = 0;
+    if (b < nseg) {
+      Seg s = load_seg(cu_q, cu_k, b, total_q, total_k, 0);
+      if (s.lq < 0 || s.lk < 0) set_status(&status, BS_DEV_NOT_MONOTONE);
+      else if (cu_q != nullptr && (s.lq > max_seqlen || s.lk > max_seqlen)) set_status(&status, BS_DEV_TOO_LONG);
+      else {
+        const int64_t la = kind == kPlanFwd ? s.lq : s.lk;
+        cnt = (int32_t)((la + tile_a - 1) / tile_a);
+      }
+    }
+    scan[t] = cnt;
+    __syncthreads();
+    for (int off = 1; off < kCountThreads; off <<= 1) {  // inclusive Hillis-Steele scan
+      int32_t x = t >= off ? scan[t - off] : 0;
+      __syncthreads();
+      scan[t] += x;
+      __syncthreads();
+    }
+    if (b < nseg) seg_off[b] = carry + scan[t] - cnt;
+    __syncthreads();
+    if (t == kCountThreads - 1) carry += scan[t];
+    __syncthreads();
+  }
+  if (t == 0) {
+    seg_off[nseg] = carry;
+    hdr->status = status;
+    hdr->n_items = status == 0 ? carry : 0;
+  }
+}
+
+__global__ __launch_bounds__(256) void plan_emit(
+    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int32_t num_seqs,
+    int64_t total_q, int64_t total_k, int32_t diag_chunk, int causal, int kind, int tile_a,
+    int tile_b, int64_t max_items, const WsHeader* __restrict__ hdr,
+    const int32_t* __restrict__ seg_off, WorkItem* __restrict__ items) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= max_items || i >= hdr->n_items) return;
+  const int32_t nseg = cu_q == nullptr ? 1 : num_seqs;
+  // segment b with seg_off[b] <= i < seg_off[b+1] (skipping empty segments)
+  int32_t lo = 0, hi = nseg - 1;
+  while (lo < hi) {
+    int32_t mid = (lo + hi + 1) >> 1;
+    if (seg_off[mid] <= i) lo = mid; else hi = mid - 1;
+  }
+  const int32_t b = lo;
+  const Seg s = load_seg(cu_q, cu_k, b, total_q, total_k, diag_chunk);
+  const int64_t tile = i - seg_off[b];
+  const int64_t diag = s.diag;
+  WorkItem w;
+  w.seg = b; w.tile = (int32_t)tile; w.diag = s.diag; w.pad0 = 0; w.pad1 = 0;
+  if (kind == kPlanFwd) {
+    const int64_t BM = tile_a, BN = tile_b;
+    const int64_t q_first = tile * BM;
+    const int64_t q_last = (q_first + BM < s.lq ? q_first + BM : s.lq) - 1;
+    const int64_t nkt = (s.lk + BN - 1) / BN;
+    int64_t n_tiles, n_full;
+    if (causal) {
+      const int64_t lim = q_last + diag;
+      n_tiles = lim < 0 ? 0 : (lim / BN + 1 < nkt ? lim / BN + 1 : nkt);
+      int64_t f = q_first + diag + 1;
+      f = f < s.lk ? f : s.lk;
+      n_full = f > 0 ? f / BN : 0;
+    } else {
+      n_tiles = nkt;
+      n_full = s.lk / BN;
+    }
+    w.a_start = (int32_t)(s.q0 + q_first);
+    w.a_rows = (int32_t)(q_last - q_first + 1);
+    w.b_start = (int32_t)s.k0;
+    w.b_len = (int32_t)s.lk;
+    w.n0 = (int32_t)n_full;
+    w.n1 = (int32_t)n_tiles;
+    w.n2 = (int32_t)n_tiles;  // sort key
+  } else {
+    const int64_t BM = tile_b, BN = tile_a;
+    const int64_t k_first = tile * BN;
+    const int64_t nqt = (s.lq + BM - 1) / BM;
+    const bool in_range = k_first + BN <= s.lk;
+    int64_t first, ffirst;
+    if (causal) {
+      const int64_t r = k_first - diag;  // first query row that sees key k_first
+      first = r > s.lq - 1 ? nqt : (r > 0 ? r / BM : 0);
+      if (!in_range) {
+        ffirst = nqt;
+      } else {
+        const int64_t t = k_first + BN - 1 - diag;  // FULL needs q_first >= t
+        ffirst = t <= 0 ? 0 : (t + BM - 1) / BM;
+        ffirst = ffirst < nqt ? ffirst : nqt;
+      }
+    } else {
+      first = 0;
+      ffirst = in_range ? 0 : nqt;
+    }
+    const int64_t n_vis = nqt - first;
+    const int64_t n_masked = ffirst - first > 0 ? ffirst - first : 0;
+    w.a_start = (int32_t)(s.k0 + k_first);
+    w.a_rows = (int32_t)(s.lk - k_first < BN ? s.lk - k_first : BN);
+    w.b_start = (int32_t)s.q0;
+    w.b_len = (int32_t)s.lq;
+    w.n0 = (int32_t)first;
+    w.n1 = (int32_t)n_masked;
+    w.n2 = (int32_t)n_vis;
+  }
+  items[i] = w;
+}
+
+// Sort key of an unsorted entry: forward n_tiles, backward n_vis (both in n2).
+constexpr int kSortChunk = 1024;
+
+__global__ __launch_bounds__(256) void plan_sort(int64_t max_items,
+                                                 const WsHeader* __restrict__ hdr,
+                                                 const WorkItem* __restrict__ in,
+                                                 WorkItem* __restrict__ out) {
+  __shared__ int32_t keys[kSortChunk];
+  const int64_t n = hdr->n_items;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if ((int64_t)blockIdx.x * blockDim.x >= n) return;  // whole block idle (uniform)
+  const bool live = i < n && i < max_items;
+  const int32_t mine = live ? in[i].n2 : 0;
+  int64_t rank = 0;
+  for (int64_t base = 0; base < n; base += kSortChunk) {
+    for (int j = threadIdx.x; j < kSortChunk; j += blockDim.x)
+      keys[j] = base + j < n ? in[base + j].n2 : -1;
+    __syncthreads();
+    const int64_t lim = n - base < kSortChunk ? n - base : kSortChunk;
+    for (int64_t j = 0; j < lim; ++j) {
+      const int32_t kj = keys[j];
+      rank += (kj > mine) || (kj == mine && base + j < i);
+    }
+    __syncthreads();
+  }
+  if (live) out[rank] = in[i];
+}
+
+}  // namespace
+
+hipError_t launch_plan(PlanKind kind, const int32_t* cu_q, const int32_t* cu_k, int32_t num_seqs,
+                       int64_t total_q, int64_t total_k, int32_t max_seqlen, int32_t diag_chunk,
+                       int causal, int tile_a, int tile_b, int64_t max_items, void* ws,
+                       const WsLayout& L, hipStream_t stream) {
+  char* base = static_cast<char*>(ws);
+  WsHeader* hdr = reinterpret_cast<WsHeader*>(base);
+  int32_t* seg_off = reinterpret_cast<int32_t*>(base + L.seg_off);
+  WorkItem* unsorted = reinterpret_cast<WorkItem*>(base + L.unsorted);
+  WorkItem* sorted = reinterpret_cast<WorkItem*>(base + L.sorted);
+  hipLaunchKernelGGL(plan_count, dim3(1), dim3(kCountThreads), 0, stream, cu_q, cu_k, num_seqs,
+                     total_q, total_k, max_seqlen, (int)kind, tile_a, hdr, seg_off);
+  if (max_items > 0) {
+    const unsigned blocks = (unsigned)((max_items + 255) / 256);
+    hipLaunchKernelGGL(plan_emit, dim3(blocks), dim3(256), 0, stream, cu_q, cu_k, num_seqs,
+                       total_q, total_k, diag_chunk, causal, (int)kind, tile_a, tile_b,
+                       max_items, hdr, seg_off, unsorted);
+    hipLaunchKernelGGL(plan_sort, dim3(blocks), dim3(256), 0, stream, max_items, hdr, unsorted,
+                       sorted);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace bs

@@ -1,0 +1,77 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports every
+entry point the header declares, and rejects bad arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2502_21231_amd import bs_attn as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bs_attn.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bs_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.fail("libbs_attn.so is not built (run __graft_entry__.build())")
+    return B.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) == 12, names
+    assert set(names) == set(B.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+FAKE = 4096  # a non-null, aligned address that the validation rejects before any use
+
+
+def dims(**kw):
+    d = dict(total_q=128, total_k=128, hq=4, hkv=2, head_dim=128, dtype=B.BS_BF16)
+    d.update(kw)
+    return B.bs_dims(**d)
+
+
+def fwd(lib, d, ws_bytes=1 << 30, scale=0.1, q=FAKE, cu=FAKE):
+    return lib.bs_attn_varlen_fwd(ctypes.byref(d), q, FAKE, FAKE, cu, cu, 1, 128, 1, scale, FAKE,
+                                  FAKE, FAKE, ws_bytes, None)
+
+
+def test_rejects_bad_arguments_without_device(lib):
+    assert fwd(lib, dims(head_dim=96)) == B.BS_ERR_UNSUPPORTED
+    assert "head_dim" in B.bs_last_error()
+    assert fwd(lib, dims(dtype=7)) == B.BS_ERR_UNSUPPORTED
+    assert fwd(lib, dims(hq=6, hkv=4)) == B.BS_ERR_INVALID_ARG
+    assert fwd(lib, dims(hkv=0)) == B.BS_ERR_INVALID_ARG
+    assert fwd(lib, dims(total_q=-1)) == B.BS_ERR_INVALID_ARG
+    assert fwd(lib, dims(), q=None) == B.BS_ERR_INVALID_ARG
+    assert "q is NULL" in B.bs_last_error()
+    assert fwd(lib, dims(), q=FAKE + 2) == B.BS_ERR_INVALID_ARG
+    assert fwd(lib, dims(), scale=float("nan")) == B.BS_ERR_INVALID_ARG
+    assert fwd(lib, dims(), scale=-1.0) == B.BS_ERR_INVALID_ARG
+    assert fwd(lib, dims(), cu=None) == B.BS_ERR_INVALID_ARG
+    assert fwd(lib, dims(), ws_bytes=16) == B.BS_ERR_WORKSPACE
+    assert "smaller" in B.bs_last_error()
+    d = dims()
+    assert lib.bs_lse_merge(ctypes.byref(d), FAKE, FAKE, 0, FAKE, FAKE, None) == B.BS_ERR_INVALID_ARG
+    assert lib.bs_read_device_status(None, None) == B.BS_ERR_WORKSPACE
+
+
+def test_workspace_size_grows_with_problem(lib):
+    small = B.bs_attn_workspace_size(B.BS_OP_VARLEN_FWD, dims(), 1, 128)
+    big = B.bs_attn_workspace_size(B.BS_OP_VARLEN_FWD, dims(total_q=4096, total_k=4096), 1, 4096)
+    bwd = B.bs_attn_workspace_size(B.BS_OP_VARLEN_BWD, dims(total_q=4096, total_k=4096), 1, 4096)
+    assert 0 < small < big < bwd
+    # the varlen backward holds a float32 dQ accumulator [T, hq, d] and D [hq, T]
+    assert bwd >= 4096 * 4 * 128 * 4 + 4 * 4096 * 4
+    assert lib.bs_attn_workspace_size(9, ctypes.byref(dims()), 1, 1) == 0

@@ -123,7 +123,8 @@ def time_steps(step, args, dev, flops_fwd, flops_bwd):
     total_ms = e0.elapsed_time(e1)
     kern = {}
     names = {B.BS_KERNEL_PLAN: "plan", B.BS_KERNEL_FWD: "fwd", B.BS_KERNEL_PREPROCESS: "bwd_preprocess",
-             B.BS_KERNEL_BWD: "bwd", B.BS_KERNEL_FINALIZE: "dq_finalize", B.BS_KERNEL_MERGE: "lse_merge"}
+             B.BS_KERNEL_BWD_DQ: "bwd_dq", B.BS_KERNEL_BWD_DKDV: "bwd_dkdv",
+             B.BS_KERNEL_FINALIZE: "dq_finalize", B.BS_KERNEL_MERGE: "lse_merge"}
     for kind, nm in names.items():
         ms, n = B.bs_profile_read(kind)
         if n:
@@ -134,9 +135,12 @@ def time_steps(step, args, dev, flops_fwd, flops_bwd):
     flops = flops_fwd + flops_bwd
     value = flops / (ms_step * 1e-3) / 1e12
     fwd_ms = kern.get("fwd", {}).get("ms_per_step", float("nan"))
-    bwd_ms = kern.get("bwd", {}).get("ms_per_step", float("nan"))
-    dom = "bwd" if bwd_ms >= fwd_ms else "fwd"
-    dom_flops = flops_bwd if dom == "bwd" else flops_fwd
+    bwd_ms = sum(kern.get(k, {}).get("ms_per_step", 0.0) for k in ("bwd_dq", "bwd_dkdv")) or float("nan")
+    # MFMA work each attention kernel must do, per visible pair and query head:
+    # forward S and PV (4d); dQ kernel S, dP, dQ (6d); dK/dV kernel S, dP, dV, dK (8d)
+    per_pair = {"fwd": 4, "bwd_dq": 6, "bwd_dkdv": 8}
+    dom = max((k for k in per_pair if k in kern), key=lambda k: kern[k]["ms_per_step"])
+    dom_flops = flops_fwd / 4 * per_pair[dom]
     dom_launches = kern[dom]["launches_per_step"]
     achieved = dom_flops / dom_launches / (kern[dom]["avg_ms_per_launch"] * 1e-3) / 1e12
     return {
@@ -188,7 +192,20 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="packed7b")
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run 3 plain 1 GiB device-to-device copies (the reference kernel "
+                         "that scales the HBM byte counters of a profiler run) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": 1 << 30, "copy_calibration_bytes_written": 1 << 30,
+                          "launches": 3}))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU's share of the work; --gpus {args.gpus} is not supported "
               f"(this build has no multi-GPU path: use --gpus 1)", file=sys.stderr)

@@ -119,7 +119,7 @@ int bs_attn_varlen_fwd(const bs_dims* dims, const void* q, const void* k, const 
 
 /* Varlen backward: given the forward's out and lse and the upstream gradient
  * dout, writes dq [T, hq, d], dk and dv [Tk, hkv, d] (overwritten, not added).
- * dQ is accumulated in float32 inside the workspace and rounded once. */
+ * Every gradient is accumulated in float32 and rounded once. */
 int bs_attn_varlen_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,
                        const void* out, const float* lse, const void* dout,
                        const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
@@ -185,13 +185,14 @@ int bs_attn_plan_export(int op, const bs_dims* dims, const int32_t* cu_seqlens_q
 
 /* Kernel classes timed by the profiling hooks below. */
 enum {
-  BS_KERNEL_PLAN = 0,       /* the three planning kernels of a call */
+  BS_KERNEL_PLAN = 0,       /* the three planning kernels of a plan */
   BS_KERNEL_FWD = 1,        /* forward attention kernel */
   BS_KERNEL_PREPROCESS = 2, /* backward preprocess (D = rowsum(dO * O)) */
-  BS_KERNEL_BWD = 3,        /* backward attention kernel(s) */
-  BS_KERNEL_FINALIZE = 4,   /* dQ accumulator -> dq */
-  BS_KERNEL_MERGE = 5,      /* LSE merge */
-  BS_KERNEL_COUNT = 6
+  BS_KERNEL_BWD_DQ = 3,     /* backward kernel producing dQ */
+  BS_KERNEL_BWD_DKDV = 4,   /* backward kernel producing dK and dV */
+  BS_KERNEL_FINALIZE = 5,   /* float32 dQ accumulator -> dq */
+  BS_KERNEL_MERGE = 6,      /* LSE merge */
+  BS_KERNEL_COUNT = 7
 };
 
 /* Profiling (off by default, process-wide).  While enabled, every call

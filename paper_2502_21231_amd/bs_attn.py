@@ -26,7 +26,8 @@ EXPORTS = (
     "bs_attn_chunk_bwd", "bs_dq_finalize", "bs_lse_merge", "bs_read_device_status",
     "bs_attn_plan_export", "bs_set_profiling", "bs_profile_read", "bs_last_error",
 )
-BS_KERNEL_PLAN, BS_KERNEL_FWD, BS_KERNEL_PREPROCESS, BS_KERNEL_BWD, BS_KERNEL_FINALIZE, BS_KERNEL_MERGE = range(6)
+(BS_KERNEL_PLAN, BS_KERNEL_FWD, BS_KERNEL_PREPROCESS, BS_KERNEL_BWD_DQ, BS_KERNEL_BWD_DKDV,
+ BS_KERNEL_FINALIZE, BS_KERNEL_MERGE) = range(7)
 
 
 class BsError(RuntimeError):

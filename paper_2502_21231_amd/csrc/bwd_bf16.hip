@@ -1,24 +1,34 @@
 // bf16 attention backward for gfx950 (recomputes P from the saved LSE).
 //
-// One workgroup = one key tile of the backward work list (kBwdBN = 128 keys)
-// for one KV head; 4 waves, wave w owning keys 32w .. 32w+31, whose K and V
-// rows it keeps in registers and whose dK, dV it accumulates in registers over
-// all query heads of the KV group and all visible query tiles (kBwdBM = 64
-// rows), the MASKED (diagonal) query tiles first.  Per query tile:
+// Two kernels, neither of which needs atomics:
 //
-//   S  = Q K^T            (MFMA, A = Q from LDS, B = K from registers)
-//   dP = dO V^T           (MFMA, A = dO from LDS, B = V from registers)
-//   P  = exp2(S*scale*log2e - LSE*log2e),  dS = P (dP - D)        (fp32)
-//   dV^T += dO^T P        (A = dO^T from LDS, B = P straight from registers)
-//   dK^T += Q^T dS        (A = Q^T from LDS,  B = dS straight from registers)
-//   dQ  += dS K           (dS through LDS, K^T from LDS), fp32 atomics to HBM
+// dq_bf16_kernel (query-major, walks the forward work list: 128-row query
+//   tiles over 64-key tiles).  Like the forward it keeps one query per lane,
+//   computing S^T = K Q^T and dP^T = V dO^T with Q and dO resident in
+//   registers (B operands) and K, V staged row-major in LDS (A operands);
+//   P = exp2(S*scale*log2e - LSE*log2e), dS = P (dP - D) are per-lane fp32
+//   math; dQ^T += K^T dS^T takes dS^T straight from registers as the B operand
+//   and K^T from the same row-major K tile through transposing LDS reads
+//   (ds_read_b64_tr_b16), which deliver the keys in the register order of dS^T.
+//   dQ is finished in registers and written once (bf16), or added to a float32
+//   accumulator for the context-parallel steps.
 //
-// The MFMA result layout (lane = one column, 16 rows) lets P and dS serve as
-// the B operand of the q-contractions directly; the matching permutation of the
-// q index inside each 16-group is applied when Q^T and dO^T are written to LDS.
-// Query rows past the segment load as zeros with LSE = +inf (P = 0); rows whose
-// LSE is -inf (no visible key) also get P = 0.  Keys past the segment load as
-// zeros, so they add nothing to dQ; their dK, dV are never stored.
+// dkdv_bf16_kernel (key-major, walks the backward work list: 128-key tiles
+//   over 64-row query tiles).  Wave w owns keys 32w .. 32w+31, keeps their K
+//   and V rows in registers and accumulates their dK, dV in registers over all
+//   query heads of the KV group and all visible query tiles (MASKED diagonal
+//   tiles first):
+//     S  = Q K^T,  dP = dO V^T     (A = Q, dO row reads from LDS; B = K, V registers)
+//     P, dS                         (lane = one key, 16 query rows per block)
+//     dV^T += dO^T P,  dK^T += Q^T dS   (A = transposing reads of the same Q, dO
+//                                       tiles; B = P, dS straight from registers)
+//   Query tiles are double-buffered in LDS: the next one is fetched into
+//   registers and written to the other buffer while the current one is
+//   consumed, one barrier per tile.  Query rows past the segment use
+//   LSE = +inf (P = 0), rows whose LSE is -inf (no visible key) also get P = 0.
+//
+// All LDS staging is row-contiguous 16-byte traffic (no bank conflicts); rows
+// past a segment are fetched from its last valid row and never contribute.
 #include "common.hpp"
 
 namespace bs {
@@ -31,7 +41,8 @@ struct BwdParams {
   const bf16* dout;
   const float* lse;
   const float* dvec;
-  float* dq_acc;
+  bf16* dq;          // varlen: dQ written directly
+  float* dq_acc;     // chunk: dQ added into a float32 accumulator (dq == nullptr)
   bf16* dk;
   bf16* dv;
   const WsHeader* hdr;
@@ -42,80 +53,200 @@ struct BwdParams {
   float scale, scale_log2;
 };
 
-__device__ __forceinline__ int qperm4(int g4) { return (g4 == 1) ? 2 : (g4 == 2 ? 1 : g4); }
-
-__device__ __forceinline__ int kvhead_of(int slot, int hkv) {
-  return (hkv & 7) == 0 ? (slot & 7) * (hkv >> 3) + (slot >> 3) : slot;
+__device__ __forceinline__ int spread_head(int slot, int n) {
+  return (n & 7) == 0 ? (slot & 7) * (n >> 3) + (slot >> 3) : slot;
 }
 
+// ----------------------------------------------------------------------------- dQ
 template <int D>
-__global__ __launch_bounds__(256) void bwd_bf16_kernel(const BwdParams p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void dq_bf16_kernel(const BwdParams p) {
+  constexpr int BM = kFwdBM, BN = kFwdBN;
+  constexpr int NSTR = D + 8;   // K, V row-major tiles
+  constexpr int KK = D / 16, DB = D / 32;
+  constexpr int UNITS = BN * D / 8 / 256;  // 16-byte loads per thread per tensor
+  static_assert(BM == 128 && BN == 64 && UNITS >= 1, "tile shape");
+
+  __shared__ __attribute__((aligned(16))) bf16 Ks[BN * NSTR];
+  __shared__ __attribute__((aligned(16))) bf16 Vs[BN * NSTR];
+
+  const int item_idx = blockIdx.x / p.hq;
+  if (item_idx >= p.hdr->n_items) return;
+  const WorkItem it = p.items[item_idx];
+  const int h = spread_head(blockIdx.x % p.hq, p.hq);
+  const int hk = h / p.group;
+
+  const int tid = threadIdx.x;
+  const int w = tid >> 6, lane = tid & 63, c = lane & 31, hh = lane >> 5;
+  const int qrow = w * 32 + c;
+  const bool qvalid = qrow < it.a_rows;
+  const int64_t qstride = (int64_t)p.hq * D;
+  const int kvstride = p.hkv * D;
+  const int64_t qoff = (int64_t)(it.a_start + (qvalid ? qrow : 0)) * qstride + (int64_t)h * D;
+
+  bf16x8 qf[KK], dof[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    qf[kk] = *reinterpret_cast<const bf16x8*>(p.q + qoff + kk * 16 + hh * 8);
+    dof[kk] = *reinterpret_cast<const bf16x8*>(p.dout + qoff + kk * 16 + hh * 8);
+  }
+  float lse2 = INFINITY, dval = 0.f;
+  if (qvalid) {
+    const float l = p.lse[(int64_t)h * p.total_q + it.a_start + qrow];
+    lse2 = l == -INFINITY ? INFINITY : l * kLog2e;
+    dval = p.dvec[(int64_t)h * p.total_q + it.a_start + qrow];
+  }
+  wait_vmem_all();
+
+  const bf16* kbase = p.k + (int64_t)it.b_start * kvstride + (int64_t)hk * D;
+  const bf16* vbase = p.v + (int64_t)it.b_start * kvstride + (int64_t)hk * D;
+  const int k_len = it.b_len;
+  const int n_tiles = it.n1, n_full = it.n0;
+
+  bf16x8 kreg[UNITS], vreg[UNITS];
+  auto load_tile = [&](int t) {
+    const int k0 = t * BN;
+    const int last = k_len - 1 - k0;
+    const bf16* kt = kbase + (int64_t)k0 * kvstride;
+    const bf16* vt = vbase + (int64_t)k0 * kvstride;
+#pragma unroll
+    for (int i = 0; i < UNITS; ++i) {
+      const int idx = i * 256 + tid;
+      const int row = idx / (D / 8), ch = idx % (D / 8);
+      const int r = row < last ? row : last;
+      kreg[i] = *reinterpret_cast<const bf16x8*>(kt + r * kvstride + ch * 8);
+      vreg[i] = *reinterpret_cast<const bf16x8*>(vt + r * kvstride + ch * 8);
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < UNITS; ++i) {
+      const int idx = i * 256 + tid;
+      const int row = idx / (D / 8), ch = idx % (D / 8);
+      *reinterpret_cast<bf16x8*>(&Ks[row * NSTR + ch * 8]) = kreg[i];
+      *reinterpret_cast<bf16x8*>(&Vs[row * NSTR + ch * 8]) = vreg[i];
+    }
+  };
+  const bf16* ktr = tr_lane_ptr(Ks, NSTR, 0, 0, lane);  // K^T operand reads
+
+  f32x16 dqacc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) dqacc[db] = f32x16{};
+  const float c2 = p.scale_log2;
+  const int q_rel = it.tile * BM + qrow;
+  int lim_base = k_len;
+  if (p.causal) lim_base = min(k_len, q_rel + it.diag + 1);
+  lim_base -= hh * 4;
+
+  if (n_tiles > 0) load_tile(0);
+  for (int t = 0; t < n_tiles; ++t) {
+    __syncthreads();  // previous tile consumed
+    store_tile();
+    __syncthreads();
+    if (t + 1 < n_tiles) load_tile(t + 1);
+
+    f32x16 sacc[2] = {f32x16{}, f32x16{}};
+    f32x16 dpacc[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const int off = (kb * 32 + c) * NSTR + kk * 16 + hh * 8;
+        bf16x8 a = *reinterpret_cast<const bf16x8*>(&Ks[off]);
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], sacc[kb], 0, 0, 0);
+        bf16x8 b = *reinterpret_cast<const bf16x8*>(&Vs[off]);
+        dpacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, dof[kk], dpacc[kb], 0, 0, 0);
+      }
+    }
+    if (t >= n_full) {
+      const int lim = lim_base - t * BN;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          sacc[kb][r] = (kb * 32 + (r >> 2) * 8 + (r & 3)) < lim ? sacc[kb][r] : -INFINITY;
+    }
+    bf16x8 dsb[4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float pr = fast_exp2(fmaf(sacc[kb][r], c2, -lse2));
+        dsb[kb * 2 + (r >> 3)][r & 7] = f2bf(pr * (dpacc[kb][r] - dval));
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const bf16x8 a = lds_read_tr(ktr + ks * 16 * NSTR + db * 32, NSTR);
+        dqacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[ks], dqacc[db], 0, 0, 0);
+      }
+    }
+  }
+
+  if (qvalid) {
+    const int64_t off = (int64_t)(it.a_start + qrow) * qstride + (int64_t)h * D + hh * 4;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const int col = db * 32 + a * 8;
+        if (p.dq != nullptr) {
+          bf16x4 x = {f2bf(dqacc[db][a * 4 + 0] * p.scale), f2bf(dqacc[db][a * 4 + 1] * p.scale),
+                      f2bf(dqacc[db][a * 4 + 2] * p.scale), f2bf(dqacc[db][a * 4 + 3] * p.scale)};
+          *reinterpret_cast<bf16x4*>(p.dq + off + col) = x;
+        } else {
+          f32x4* dst = reinterpret_cast<f32x4*>(p.dq_acc + off + col);
+          f32x4 y = *dst;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) y[i] += dqacc[db][a * 4 + i] * p.scale;
+          *dst = y;
+        }
+      }
+    }
+  }
+}
+
+// --------------------------------------------------------------------------- dK, dV
+template <int D>
+__global__ __launch_bounds__(256) void dkdv_bf16_kernel(const BwdParams p) {
   constexpr int BM = kBwdBM, BN = kBwdBN;
   constexpr int KK = D / 16, DB = D / 32;
-  constexpr int NSTR = D + 8;      // row-major [row][d] tiles
-  constexpr int TSTR = BM + 8;     // transposed [d][q] tiles
-  constexpr int SSTR = BN + 8;     // dS [q][key]
-  constexpr int KTSTR = BN + 8;    // K^T [d][key]
-  constexpr int QUNITS = (BM / 4) * (D / 8);   // (4 rows x 8 dims) units per Q/dO tile
-  constexpr int KUNITS = (BN / 4) * (D / 8);
-  static_assert(BM == 64 && BN == 128, "tile shape");
+  constexpr int NSTR = D + 8;                 // row-major [q][d] tiles
+  constexpr int TILE = BM * NSTR;
+  constexpr int UNITS = BM * D / 8 / 256;     // 16-byte loads per thread per tensor
+  static_assert(BM == 64 && BN == 128 && UNITS >= 1, "tile shape");
 
-  __shared__ __attribute__((aligned(16))) bf16 Qs[BM * NSTR];
-  __shared__ __attribute__((aligned(16))) bf16 dOs[BM * NSTR];
-  __shared__ __attribute__((aligned(16))) bf16 Qt[D * TSTR];
-  __shared__ __attribute__((aligned(16))) bf16 dOt[D * TSTR];
-  __shared__ __attribute__((aligned(16))) bf16 dSs[BM * SSTR];
-  __shared__ __attribute__((aligned(16))) bf16 Kt[D * KTSTR];
-  __shared__ __attribute__((aligned(16))) float lse_s[BM];
-  __shared__ __attribute__((aligned(16))) float dvec_s[BM];
+  __shared__ __attribute__((aligned(16))) bf16 Qs[2][TILE];
+  __shared__ __attribute__((aligned(16))) bf16 dOs[2][TILE];
+  __shared__ __attribute__((aligned(16))) float lse_s[2][BM];
+  __shared__ __attribute__((aligned(16))) float dvec_s[2][BM];
 
   const int item_idx = blockIdx.x / p.hkv;
   if (item_idx >= p.hdr->n_items) return;
   const WorkItem it = p.items[item_idx];
-  const int hk = kvhead_of(blockIdx.x % p.hkv, p.hkv);
+  const int hk = spread_head(blockIdx.x % p.hkv, p.hkv);
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, c = lane & 31, hh = lane >> 5;
   const int64_t qstride = (int64_t)p.hq * D;
-  const int64_t kvstride = (int64_t)p.hkv * D;
+  const int kvstride = p.hkv * D;
   const int k_rows = it.a_rows;
-  const int key_loc = w * 32 + c;                  // this lane's key inside the tile
+  const int key_loc = w * 32 + c;
   const bool kvalid = key_loc < k_rows;
-  const int key_rel = it.tile * BN + key_loc;      // key index inside its segment
-  const int k_len_seg = it.tile * BN + k_rows;     // keys before the end of this tile's segment part
+  const int key_rel = it.tile * BN + key_loc;   // key index inside its segment
 
-  // this lane's K and V rows (B operands of S = Q K^T and dP = dO V^T)
   bf16x8 kf[KK], vf[KK];
   {
-    const int64_t row = it.a_start + (kvalid ? key_loc : 0);
-    const bf16* kp = p.k + row * kvstride + (int64_t)hk * D;
-    const bf16* vp = p.v + row * kvstride + (int64_t)hk * D;
+    const int64_t off = (int64_t)(it.a_start + (kvalid ? key_loc : 0)) * kvstride + (int64_t)hk * D + hh * 8;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      bf16x8 a = *reinterpret_cast<const bf16x8*>(kp + kk * 16 + hh * 8);
-      bf16x8 b = *reinterpret_cast<const bf16x8*>(vp + kk * 16 + hh * 8);
-      kf[kk] = kvalid ? a : bf16x8{};
-      vf[kk] = kvalid ? b : bf16x8{};
+      kf[kk] = *reinterpret_cast<const bf16x8*>(p.k + off + kk * 16);
+      vf[kk] = *reinterpret_cast<const bf16x8*>(p.v + off + kk * 16);
     }
   }
-  // K^T of the whole tile in LDS (natural key order), B operand of dQ = dS K
-  for (int u = tid; u < KUNITS; u += 256) {
-    const int g = u % (BN / 4), ch = u / (BN / 4);
-    bf16x8 r[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = g * 4 + i;
-      const bool ok = row < k_rows;
-      bf16x8 x = *reinterpret_cast<const bf16x8*>(p.k + (int64_t)(it.a_start + (ok ? row : 0)) * kvstride +
-                                                  (int64_t)hk * D + ch * 8);
-      r[i] = ok ? x : bf16x8{};
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      bf16x4 col = {r[0][e], r[1][e], r[2][e], r[3][e]};
-      *reinterpret_cast<bf16x4*>(&Kt[(ch * 8 + e) * KTSTR + g * 4]) = col;
-    }
-  }
+  wait_vmem_all();
 
   f32x16 dvacc[DB], dkacc[DB];
 #pragma unroll
@@ -124,134 +255,124 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const BwdParams p) {
   const int q_len = it.b_len;
   const int qt_first = it.n0, n_masked = it.n1, n_vis = it.n2;
   const int diag = it.diag;
-  // dQ block of this wave: query block qb_w, head-dim blocks dbw0 .. dbw0 + DBW - 1
-  constexpr int DBW = DB / 2;
-  const int qb_w = w & 1, dbw0 = (w >> 1) * DBW;
+  const int n_iter = n_vis * p.group;
 
-  for (int hg = 0; hg < p.group; ++hg) {
+  bf16x8 rq[UNITS], rd[UNITS];
+  float lse_r = INFINITY, dv_r = 0.f;
+  auto load_tile = [&](int i) {
+    const int hg = i / n_vis, j = i - hg * n_vis;
     const int h = hk * p.group + hg;
-    for (int j = 0; j < n_vis; ++j) {
-      const int qt = qt_first + j;
-      const int q_rel0 = qt * BM;
-      const int64_t q_glob0 = (int64_t)it.b_start + q_rel0;
-      const bool masked = j < n_masked;
-
-      __syncthreads();  // previous tile fully consumed
-      // Q and dO tiles: row-major and transposed (q permuted in 16-groups)
-      for (int u = tid; u < QUNITS; u += 256) {
-        const int g = u / (D / 8), ch = u % (D / 8);
-        bf16x8 rq[4], rd[4];
+    const int q_rel0 = (qt_first + j) * BM;
+    const int64_t q_glob0 = (int64_t)it.b_start + q_rel0;
+    const int last = q_len - 1 - q_rel0;
+    const bf16* qp = p.q + q_glob0 * qstride + (int64_t)h * D;
+    const bf16* dp = p.dout + q_glob0 * qstride + (int64_t)h * D;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = g * 4 + i;
-          const bool ok = q_rel0 + row < q_len;
-          const int64_t off = (q_glob0 + (ok ? row : 0)) * qstride + (int64_t)h * D + ch * 8;
-          bf16x8 a = *reinterpret_cast<const bf16x8*>(p.q + off);
-          bf16x8 b = *reinterpret_cast<const bf16x8*>(p.dout + off);
-          rq[i] = ok ? a : bf16x8{};
-          rd[i] = ok ? b : bf16x8{};
-          *reinterpret_cast<bf16x8*>(&Qs[row * NSTR + ch * 8]) = rq[i];
-          *reinterpret_cast<bf16x8*>(&dOs[row * NSTR + ch * 8]) = rd[i];
-        }
-        const int pcol = (g >> 2) * 16 + qperm4(g & 3) * 4;
+    for (int u = 0; u < UNITS; ++u) {
+      const int idx = u * 256 + tid;
+      const int row = idx / (D / 8), ch = idx % (D / 8);
+      const int64_t ro = (int64_t)(row < last ? row : last) * qstride + ch * 8;
+      rq[u] = *reinterpret_cast<const bf16x8*>(qp + ro);
+      rd[u] = *reinterpret_cast<const bf16x8*>(dp + ro);
+    }
+    if (tid < BM) {
+      const bool ok = tid <= last;
+      const int64_t li = (int64_t)h * p.total_q + q_glob0 + (ok ? tid : 0);
+      const float l = p.lse[li];
+      lse_r = (!ok || l == -INFINITY) ? INFINITY : l * kLog2e;
+      dv_r = ok ? p.dvec[li] : 0.f;
+    }
+  };
+  auto store_tile = [&](int buf) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          bf16x4 cq = {rq[0][e], rq[1][e], rq[2][e], rq[3][e]};
-          bf16x4 cd = {rd[0][e], rd[1][e], rd[2][e], rd[3][e]};
-          *reinterpret_cast<bf16x4*>(&Qt[(ch * 8 + e) * TSTR + pcol]) = cq;
-          *reinterpret_cast<bf16x4*>(&dOt[(ch * 8 + e) * TSTR + pcol]) = cd;
-        }
-      }
-      if (tid < BM) {
-        const bool ok = q_rel0 + tid < q_len;
-        float l = ok ? p.lse[(int64_t)h * p.total_q + q_glob0 + tid] : INFINITY;
-        lse_s[tid] = l == -INFINITY ? INFINITY : l * kLog2e;
-        dvec_s[tid] = ok ? p.dvec[(int64_t)h * p.total_q + q_glob0 + tid] : 0.f;
-      }
-      __syncthreads();
+    for (int u = 0; u < UNITS; ++u) {
+      const int idx = u * 256 + tid;
+      const int row = idx / (D / 8), ch = idx % (D / 8);
+      *reinterpret_cast<bf16x8*>(&Qs[buf][row * NSTR + ch * 8]) = rq[u];
+      *reinterpret_cast<bf16x8*>(&dOs[buf][row * NSTR + ch * 8]) = rd[u];
+    }
+    if (tid < BM) {
+      lse_s[buf][tid] = lse_r;
+      dvec_s[buf][tid] = dv_r;
+    }
+  };
+  const int tro = tr_lane_ptr(Qs[0], NSTR, 0, 0, lane) - Qs[0];  // transposing-read offset
 
-      f32x16 sacc[2], dpacc[2];
+  if (n_iter > 0) {
+    load_tile(0);
+    store_tile(0);
+    if (n_iter > 1) load_tile(1);
+  }
+  __syncthreads();
+
+  for (int i = 0; i < n_iter; ++i) {
+    const int buf = i & 1;
+    const int hg = i / n_vis, j = i - hg * n_vis;
+    const int q_rel0 = (qt_first + j) * BM;
+    const bool masked = j < n_masked;
+    const bf16* Qb = Qs[buf];
+    const bf16* dOb = dOs[buf];
+
+    f32x16 sacc[2] = {f32x16{}, f32x16{}};
+    f32x16 dpacc[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
-        sacc[qb] = f32x16{};
-        dpacc[qb] = f32x16{};
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          bf16x8 a = *reinterpret_cast<const bf16x8*>(&Qs[(qb * 32 + c) * NSTR + kk * 16 + hh * 8]);
-          sacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kf[kk], sacc[qb], 0, 0, 0);
-          bf16x8 b = *reinterpret_cast<const bf16x8*>(&dOs[(qb * 32 + c) * NSTR + kk * 16 + hh * 8]);
-          dpacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, vf[kk], dpacc[qb], 0, 0, 0);
-        }
+        const int off = (qb * 32 + c) * NSTR + kk * 16 + hh * 8;
+        bf16x8 a = *reinterpret_cast<const bf16x8*>(&Qb[off]);
+        sacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kf[kk], sacc[qb], 0, 0, 0);
+        bf16x8 b = *reinterpret_cast<const bf16x8*>(&dOb[off]);
+        dpacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, vf[kk], dpacc[qb], 0, 0, 0);
       }
+    }
 
-      bf16x8 pb[4], dsb[4];
+    bf16x8 pb[4], dsb[4];
+    // lane = key key_loc, rows q = qb*32 + a4*8 + hh*4 + e
+    const int vis_lim = key_rel - diag - q_rel0 - hh * 4;  // visible iff row_local >= vis_lim
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < 2; ++qb) {
 #pragma unroll
-        for (int a4 = 0; a4 < 4; ++a4) {
-          const int ql = qb * 32 + a4 * 8 + hh * 4;  // 4 consecutive query rows
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse_s[ql]);
-          const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dvec_s[ql]);
+      for (int a4 = 0; a4 < 4; ++a4) {
+        const int ql = qb * 32 + a4 * 8 + hh * 4;
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse_s[buf][ql]);
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dvec_s[buf][ql]);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = a4 * 4 + i;
-            float pr = fast_exp2(sacc[qb][r] * p.scale_log2 - l4[i]);
-            if (masked) {
-              const int qrel = q_rel0 + ql + i;
-              const bool vis = key_rel < k_len_seg && (!p.causal || key_rel - qrel <= diag);
-              pr = vis ? pr : 0.f;
-            }
-            const float ds = pr * (dpacc[qb][r] - d4[i]);
-            pb[qb * 2 + (r >> 3)][r & 7] = f2bf(pr);
-            const bf16 dsh = f2bf(ds);
-            dsb[qb * 2 + (r >> 3)][r & 7] = dsh;
-            dSs[(ql + i) * SSTR + key_loc] = dsh;
-          }
-        }
-      }
-
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-#pragma unroll
-        for (int qs = 0; qs < 4; ++qs) {
-          bf16x8 a = *reinterpret_cast<const bf16x8*>(&dOt[(db * 32 + c) * TSTR + qs * 16 + hh * 8]);
-          dvacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[qs], dvacc[db], 0, 0, 0);
-          bf16x8 b = *reinterpret_cast<const bf16x8*>(&Qt[(db * 32 + c) * TSTR + qs * 16 + hh * 8]);
-          dkacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, dsb[qs], dkacc[db], 0, 0, 0);
-        }
-      }
-      __syncthreads();  // dS tile complete
-
-      f32x16 dqacc[DBW];
-#pragma unroll
-      for (int i = 0; i < DBW; ++i) dqacc[i] = f32x16{};
-#pragma unroll
-      for (int kk = 0; kk < BN / 16; ++kk) {
-        bf16x8 a = *reinterpret_cast<const bf16x8*>(&dSs[(qb_w * 32 + c) * SSTR + kk * 16 + hh * 8]);
-#pragma unroll
-        for (int i = 0; i < DBW; ++i) {
-          bf16x8 b = *reinterpret_cast<const bf16x8*>(&Kt[((dbw0 + i) * 32 + c) * KTSTR + kk * 16 + hh * 8]);
-          dqacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, dqacc[i], 0, 0, 0);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < DBW; ++i) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int ql = qb_w * 32 + (r >> 2) * 8 + hh * 4 + (r & 3);
-          if (q_rel0 + ql < q_len) {
-            float* dst = p.dq_acc + (q_glob0 + ql) * qstride + (int64_t)h * D + (dbw0 + i) * 32 + c;
-            unsafeAtomicAdd(dst, dqacc[i][r] * p.scale);
-          }
+        for (int e = 0; e < 4; ++e) {
+          const int r = a4 * 4 + e;
+          float pr = fast_exp2(fmaf(sacc[qb][r], p.scale_log2, -l4[e]));
+          if (masked && p.causal) pr = (qb * 32 + a4 * 8 + e) >= vis_lim ? pr : 0.f;
+          pb[qb * 2 + (r >> 3)][r & 7] = f2bf(pr);
+          dsb[qb * 2 + (r >> 3)][r & 7] = f2bf(pr * (dpacc[qb][r] - d4[e]));
         }
       }
     }
+
+    const bf16* dOt = dOb + tro;
+    const bf16* Qt = Qb + tro;
+#pragma unroll
+    for (int qs = 0; qs < 4; ++qs) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const int off = qs * 16 * NSTR + db * 32;
+        const bf16x8 a = lds_read_tr(dOt + off, NSTR);
+        dvacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[qs], dvacc[db], 0, 0, 0);
+        const bf16x8 b = lds_read_tr(Qt + off, NSTR);
+        dkacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, dsb[qs], dkacc[db], 0, 0, 0);
+      }
+    }
+
+    if (i + 1 < n_iter) {
+      store_tile(buf ^ 1);  // buffer buf^1 was last read in iteration i-1
+      if (i + 2 < n_iter) load_tile(i + 2);
+    }
+    __syncthreads();
   }
 
   if (kvalid) {
     const int64_t row = it.a_start + key_loc;
-    bf16* dkp = p.dk + row * kvstride + (int64_t)hk * D;
-    bf16* dvp = p.dv + row * kvstride + (int64_t)hk * D;
+    bf16* dkp = p.dk + row * kvstride + (int64_t)hk * D + hh * 4;
+    bf16* dvp = p.dv + row * kvstride + (int64_t)hk * D + hh * 4;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -260,30 +381,23 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const BwdParams p) {
                      f2bf(dkacc[db][a * 4 + 2] * p.scale), f2bf(dkacc[db][a * 4 + 3] * p.scale)};
         bf16x4 xv = {f2bf(dvacc[db][a * 4 + 0]), f2bf(dvacc[db][a * 4 + 1]),
                      f2bf(dvacc[db][a * 4 + 2]), f2bf(dvacc[db][a * 4 + 3])};
-        *reinterpret_cast<bf16x4*>(dkp + db * 32 + a * 8 + hh * 4) = xk;
-        *reinterpret_cast<bf16x4*>(dvp + db * 32 + a * 8 + hh * 4) = xv;
+        *reinterpret_cast<bf16x4*>(dkp + db * 32 + a * 8) = xk;
+        *reinterpret_cast<bf16x4*>(dvp + db * 32 + a * 8) = xv;
       }
     }
   }
 }
 
-}  // namespace
-
-hipError_t launch_bwd_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
-                           const void* dout, const float* lse, const float* dvec, float* dq_acc,
-                           int causal, float scale, void* dk, void* dv, const void* ws,
-                           const WsLayout& L, hipStream_t stream) {
-  if (L.max_items == 0 || dims.hkv == 0) return hipSuccess;
-  BwdParams p;
+BwdParams make_params(const bs_dims& dims, const void* q, const void* k, const void* v,
+                      const void* dout, const float* lse, const float* dvec, int causal,
+                      float scale, const void* ws, const WsLayout& L) {
+  BwdParams p = {};
   p.q = static_cast<const bf16*>(q);
   p.k = static_cast<const bf16*>(k);
   p.v = static_cast<const bf16*>(v);
   p.dout = static_cast<const bf16*>(dout);
   p.lse = lse;
   p.dvec = dvec;
-  p.dq_acc = dq_acc;
-  p.dk = static_cast<bf16*>(dk);
-  p.dv = static_cast<bf16*>(dv);
   p.hdr = static_cast<const WsHeader*>(ws);
   p.items = reinterpret_cast<const WorkItem*>(static_cast<const char*>(ws) + L.sorted);
   p.total_q = dims.total_q;
@@ -293,11 +407,40 @@ hipError_t launch_bwd_bf16(const bs_dims& dims, const void* q, const void* k, co
   p.causal = causal;
   p.scale = scale;
   p.scale_log2 = scale * kLog2e;
+  return p;
+}
+
+}  // namespace
+
+hipError_t launch_dq_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
+                          const void* dout, const float* lse, const float* dvec, int causal,
+                          float scale, void* dq, float* dq_acc, const void* ws, const WsLayout& L,
+                          hipStream_t stream) {
+  if (L.max_items == 0 || dims.hq == 0) return hipSuccess;
+  BwdParams p = make_params(dims, q, k, v, dout, lse, dvec, causal, scale, ws, L);
+  p.dq = static_cast<bf16*>(dq);
+  p.dq_acc = dq_acc;
+  const dim3 grid((unsigned)(L.max_items * dims.hq));
+  if (dims.head_dim == 128)
+    hipLaunchKernelGGL(dq_bf16_kernel<128>, grid, dim3(256), 0, stream, p);
+  else
+    hipLaunchKernelGGL(dq_bf16_kernel<64>, grid, dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_dkdv_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
+                            const void* dout, const float* lse, const float* dvec, int causal,
+                            float scale, void* dk, void* dv, const void* ws, const WsLayout& L,
+                            hipStream_t stream) {
+  if (L.max_items == 0 || dims.hkv == 0) return hipSuccess;
+  BwdParams p = make_params(dims, q, k, v, dout, lse, dvec, causal, scale, ws, L);
+  p.dk = static_cast<bf16*>(dk);
+  p.dv = static_cast<bf16*>(dv);
   const dim3 grid((unsigned)(L.max_items * dims.hkv));
   if (dims.head_dim == 128)
-    hipLaunchKernelGGL(bwd_bf16_kernel<128>, grid, dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(dkdv_bf16_kernel<128>, grid, dim3(256), 0, stream, p);
   else
-    hipLaunchKernelGGL(bwd_bf16_kernel<64>, grid, dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(dkdv_bf16_kernel<64>, grid, dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -92,17 +92,18 @@ struct PlanCfg {
 bool is_bwd(int op) { return op == BS_OP_VARLEN_BWD || op == BS_OP_CHUNK_BWD; }
 bool is_varlen(int op) { return op == BS_OP_VARLEN_FWD || op == BS_OP_VARLEN_BWD; }
 
-// Plans an op runs, in launch order (float32 backward plans twice: query tiles
-// for dQ, then key tiles for dK/dV).
+// Plans an op runs, in launch order: the forward walks query tiles; the
+// backward plans twice, query tiles for its dQ kernel, then key tiles for its
+// dK/dV kernel.
 int plans_of(int op, int dtype, PlanCfg out[2]) {
   if (dtype == BS_BF16) {
-    out[0] = is_bwd(op) ? PlanCfg{kPlanBwd, kBwdBN, kBwdBM} : PlanCfg{kPlanFwd, kFwdBM, kFwdBN};
-    return 1;
+    out[0] = PlanCfg{kPlanFwd, kFwdBM, kFwdBN};
+    out[1] = PlanCfg{kPlanBwd, kBwdBN, kBwdBM};
+  } else {
+    out[0] = PlanCfg{kPlanFwd, kF32BM, kF32BN};
+    out[1] = PlanCfg{kPlanBwd, kF32BN, kF32BM};
   }
-  out[0] = PlanCfg{kPlanFwd, kF32BM, kF32BN};
-  if (!is_bwd(op)) return 1;
-  out[1] = PlanCfg{kPlanBwd, kF32BN, kF32BM};
-  return 2;
+  return is_bwd(op) ? 2 : 1;
 }
 
 int64_t max_items_of(const PlanCfg& c, const bs_dims& d, int64_t nseg, bool varlen) {
@@ -161,7 +162,7 @@ WsLayout layout_of(int op, const bs_dims& d, int64_t nseg) {
   if (is_bwd(op)) {
     L.dvec = off;
     off += align256(sizeof(float) * (size_t)(d.hq * d.total_q));
-    if (varlen) {
+    if (varlen && d.dtype == BS_F32) {  // the float32 dQ kernel accumulates
       L.dq_acc = off;
       off += align256(sizeof(float) * (size_t)(d.total_q * d.hq * d.head_dim));
     }
@@ -272,7 +273,8 @@ int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* base = static_cast<char*>(ws);
   float* dvec = reinterpret_cast<float*>(base + L.dvec);
-  float* acc = varlen ? reinterpret_cast<float*>(base + L.dq_acc) : dq_accum;
+  const bool f32 = d.dtype == BS_F32;
+  float* acc = varlen ? (f32 ? reinterpret_cast<float*>(base + L.dq_acc) : nullptr) : dq_accum;
   WsLayout Lp;
   {
     ProfScope ps(BS_KERNEL_PLAN, s);
@@ -281,29 +283,34 @@ int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
   }
   {
     ProfScope ps(BS_KERNEL_PREPROCESS, s);
-    BS_HIP(launch_bwd_preprocess(d, out, dout, dvec, varlen ? acc : nullptr, ws, s),
+    BS_HIP(launch_bwd_preprocess(d, out, dout, dvec, (varlen && f32) ? acc : nullptr, ws, s),
            "preprocess launch");
   }
-  if (d.dtype == BS_BF16) {
-    ProfScope ps(BS_KERNEL_BWD, s);
-    BS_HIP(launch_bwd_bf16(d, q, k, v, dout, lse, dvec, acc, causal, scale, dk, dv, ws, Lp, s),
-           "backward launch");
-  } else {
-    {
-      ProfScope ps(BS_KERNEL_BWD, s);
+  {
+    ProfScope ps(BS_KERNEL_BWD_DQ, s);
+    if (f32)
       BS_HIP(launch_bwd_f32_dq(d, q, k, v, lse, dout, dvec, causal, scale, acc, ws, Lp, s),
              "backward dQ launch");
-    }
-    {
-      ProfScope ps(BS_KERNEL_PLAN, s);
-      BS_HIP(run_plan(op, d, 1, cu_q, cu_k, num_seqs, max_seqlen, q_off, k_off, causal, ws, L, &Lp, s),
-             "planner launch");
-    }
-    ProfScope ps(BS_KERNEL_BWD, s);
-    BS_HIP(launch_bwd_f32_dkdv(d, q, k, v, lse, dout, dvec, causal, scale, dk, dv, ws, Lp, s),
-           "backward dK/dV launch");
+    else
+      BS_HIP(launch_dq_bf16(d, q, k, v, dout, lse, dvec, causal, scale, varlen ? dq : nullptr,
+                            acc, ws, Lp, s),
+             "backward dQ launch");
   }
-  if (varlen) {
+  {
+    ProfScope ps(BS_KERNEL_PLAN, s);
+    BS_HIP(run_plan(op, d, 1, cu_q, cu_k, num_seqs, max_seqlen, q_off, k_off, causal, ws, L, &Lp, s),
+           "planner launch");
+  }
+  {
+    ProfScope ps(BS_KERNEL_BWD_DKDV, s);
+    if (f32)
+      BS_HIP(launch_bwd_f32_dkdv(d, q, k, v, lse, dout, dvec, causal, scale, dk, dv, ws, Lp, s),
+             "backward dK/dV launch");
+    else
+      BS_HIP(launch_dkdv_bf16(d, q, k, v, dout, lse, dvec, causal, scale, dk, dv, ws, Lp, s),
+             "backward dK/dV launch");
+  }
+  if (varlen && f32) {
     ProfScope ps(BS_KERNEL_FINALIZE, s);
     BS_HIP(launch_dq_finalize(d, acc, dq, ws, s), "dQ finalize launch");
   }

@@ -72,6 +72,9 @@ def test_workspace_size_grows_with_problem(lib):
     big = B.bs_attn_workspace_size(B.BS_OP_VARLEN_FWD, dims(total_q=4096, total_k=4096), 1, 4096)
     bwd = B.bs_attn_workspace_size(B.BS_OP_VARLEN_BWD, dims(total_q=4096, total_k=4096), 1, 4096)
     assert 0 < small < big < bwd
-    # the varlen backward holds a float32 dQ accumulator [T, hq, d] and D [hq, T]
-    assert bwd >= 4096 * 4 * 128 * 4 + 4 * 4096 * 4
+    # the backward holds D [hq, T]; the float32 varlen backward also a dQ accumulator [T, hq, d]
+    assert bwd >= 4 * 4096 * 4
+    f32 = B.bs_attn_workspace_size(B.BS_OP_VARLEN_BWD,
+                                   dims(total_q=4096, total_k=4096, dtype=B.BS_F32), 1, 4096)
+    assert f32 >= bwd + 4096 * 4 * 128 * 4
     assert lib.bs_attn_workspace_size(9, ctypes.byref(dims()), 1, 1) == 0

@@ -14,18 +14,20 @@
 //   accumulator for the context-parallel steps.
 //
 // dkdv_bf16_kernel (key-major, walks the backward work list: 128-key tiles
-//   over 64-row query tiles).  Wave w owns keys 32w .. 32w+31, keeps their K
-//   and V rows in registers and accumulates their dK, dV in registers over all
-//   query heads of the KV group and all visible query tiles (MASKED diagonal
-//   tiles first):
-//     S  = Q K^T,  dP = dO V^T     (A = Q, dO row reads from LDS; B = K, V registers)
-//     P, dS                         (lane = one key, 16 query rows per block)
+//   over 64-row query tiles).  8 waves, 2 per SIMD: wave w owns the 32-key
+//   block w%4 of the tile and the query-row half w/4 of every query tile, and
+//   accumulates dK, dV of its keys in registers over all query heads of the KV
+//   group and all visible query tiles (MASKED diagonal tiles first):
+//     S  = Q K^T,  dP = dO V^T     (A = Q, dO rows; B = K, V rows; all from LDS)
+//     P, dS                         (lane = one key, 16 query rows)
 //     dV^T += dO^T P,  dK^T += Q^T dS   (A = transposing reads of the same Q, dO
 //                                       tiles; B = P, dS straight from registers)
-//   Query tiles are double-buffered in LDS: the next one is fetched into
-//   registers and written to the other buffer while the current one is
-//   consumed, one barrier per tile.  Query rows past the segment use
-//   LSE = +inf (P = 0), rows whose LSE is -inf (no visible key) also get P = 0.
+//   K and V of the key tile stay in LDS for the whole item; query tiles are
+//   double-buffered: the next one is fetched into registers and written to the
+//   other buffer while the current one is consumed, one barrier per tile.  At
+//   the end the two waves of each key block add their partial sums through LDS.
+//   Query rows past the segment use LSE = +inf (P = 0), rows whose LSE is -inf
+//   (no visible key) also get P = 0.
 //
 // All LDS staging is row-contiguous 16-byte traffic (no bank conflicts); rows
 // past a segment are fetched from its last valid row and never contribute.
@@ -210,18 +212,33 @@ void dq_bf16_kernel(const BwdParams p) {
 
 // --------------------------------------------------------------------------- dK, dV
 template <int D>
-__global__ __launch_bounds__(256) void dkdv_bf16_kernel(const BwdParams p) {
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void dkdv_bf16_kernel(const BwdParams p) {
   constexpr int BM = kBwdBM, BN = kBwdBN;
   constexpr int KK = D / 16, DB = D / 32;
-  constexpr int NSTR = D + 8;                 // row-major [q][d] tiles
-  constexpr int TILE = BM * NSTR;
-  constexpr int UNITS = BM * D / 8 / 256;     // 16-byte loads per thread per tensor
-  static_assert(BM == 64 && BN == 128 && UNITS >= 1, "tile shape");
-
-  __shared__ __attribute__((aligned(16))) bf16 Qs[2][TILE];
-  __shared__ __attribute__((aligned(16))) bf16 dOs[2][TILE];
-  __shared__ __attribute__((aligned(16))) float lse_s[2][BM];
-  __shared__ __attribute__((aligned(16))) float dvec_s[2][BM];
+  constexpr int NSTR = D + 8;                 // row-major [row][d] tiles
+  constexpr int QTILE = BM * NSTR;
+  constexpr int KTILE = BN * NSTR;
+  constexpr int NT = 512;
+  constexpr int QUNITS = BM * D / 8 / NT;     // 16-byte loads per thread per Q/dO tile
+  constexpr int KUNITS = BN * D / 8 / NT;     // 16-byte loads per thread per K/V tile
+  static_assert(BM == 64 && BN == 128 && QUNITS >= 1, "tile shape");
+  // LDS: K, V of the key tile (resident), Q and dO query tiles (double-buffered),
+  // LSE / D rows.  After the loop the same space holds the partial dK, dV of
+  // the waves that own the second half of each query tile.
+  constexpr int KV_BYTES = 2 * KTILE * 2;
+  constexpr int Q_BYTES = 2 * 2 * QTILE * 2;
+  constexpr int ROW_BYTES = 2 * 2 * BM * 4;
+  constexpr int RED_BYTES = 4 * 64 * 2 * DB * 16 * 4;
+  constexpr int SMEM = (KV_BYTES + Q_BYTES + ROW_BYTES) > RED_BYTES ? (KV_BYTES + Q_BYTES + ROW_BYTES)
+                                                                    : RED_BYTES;
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  bf16* Ks = reinterpret_cast<bf16*>(smem);
+  bf16* Vs = Ks + KTILE;
+  bf16* Qs = Vs + KTILE;            // [2][QTILE]
+  bf16* dOs = Qs + 2 * QTILE;       // [2][QTILE]
+  float* lse_s = reinterpret_cast<float*>(dOs + 2 * QTILE);  // [2][BM]
+  float* dvec_s = lse_s + 2 * BM;                            // [2][BM]
 
   const int item_idx = blockIdx.x / p.hkv;
   if (item_idx >= p.hdr->n_items) return;
@@ -230,23 +247,29 @@ __global__ __launch_bounds__(256) void dkdv_bf16_kernel(const BwdParams p) {
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, c = lane & 31, hh = lane >> 5;
+  const int kbw = w & 3;           // this wave's 32-key block of the tile
+  const int qh = w >> 2;           // this wave's 32-row half of every query tile
   const int64_t qstride = (int64_t)p.hq * D;
   const int kvstride = p.hkv * D;
   const int k_rows = it.a_rows;
-  const int key_loc = w * 32 + c;
-  const bool kvalid = key_loc < k_rows;
+  const int key_loc = kbw * 32 + c;
   const int key_rel = it.tile * BN + key_loc;   // key index inside its segment
 
-  bf16x8 kf[KK], vf[KK];
+  // K, V of the key tile, row-major (rows past the segment repeat its last key)
   {
-    const int64_t off = (int64_t)(it.a_start + (kvalid ? key_loc : 0)) * kvstride + (int64_t)hk * D + hh * 8;
+    const bf16* kb = p.k + (int64_t)it.a_start * kvstride + (int64_t)hk * D;
+    const bf16* vb = p.v + (int64_t)it.a_start * kvstride + (int64_t)hk * D;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      kf[kk] = *reinterpret_cast<const bf16x8*>(p.k + off + kk * 16);
-      vf[kk] = *reinterpret_cast<const bf16x8*>(p.v + off + kk * 16);
+    for (int u = 0; u < KUNITS; ++u) {
+      const int idx = u * NT + tid;
+      const int row = idx / (D / 8), ch = idx % (D / 8);
+      const int r = row < k_rows - 1 ? row : k_rows - 1;
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kb + r * kvstride + ch * 8);
+      const bf16x8 b = *reinterpret_cast<const bf16x8*>(vb + r * kvstride + ch * 8);
+      *reinterpret_cast<bf16x8*>(&Ks[row * NSTR + ch * 8]) = a;
+      *reinterpret_cast<bf16x8*>(&Vs[row * NSTR + ch * 8]) = b;
     }
   }
-  wait_vmem_all();
 
   f32x16 dvacc[DB], dkacc[DB];
 #pragma unroll
@@ -257,7 +280,7 @@ __global__ __launch_bounds__(256) void dkdv_bf16_kernel(const BwdParams p) {
   const int diag = it.diag;
   const int n_iter = n_vis * p.group;
 
-  bf16x8 rq[UNITS], rd[UNITS];
+  bf16x8 rq[QUNITS], rd[QUNITS];
   float lse_r = INFINITY, dv_r = 0.f;
   auto load_tile = [&](int i) {
     const int hg = i / n_vis, j = i - hg * n_vis;
@@ -268,8 +291,8 @@ __global__ __launch_bounds__(256) void dkdv_bf16_kernel(const BwdParams p) {
     const bf16* qp = p.q + q_glob0 * qstride + (int64_t)h * D;
     const bf16* dp = p.dout + q_glob0 * qstride + (int64_t)h * D;
 #pragma unroll
-    for (int u = 0; u < UNITS; ++u) {
-      const int idx = u * 256 + tid;
+    for (int u = 0; u < QUNITS; ++u) {
+      const int idx = u * NT + tid;
       const int row = idx / (D / 8), ch = idx % (D / 8);
       const int64_t ro = (int64_t)(row < last ? row : last) * qstride + ch * 8;
       rq[u] = *reinterpret_cast<const bf16x8*>(qp + ro);
@@ -285,18 +308,23 @@ __global__ __launch_bounds__(256) void dkdv_bf16_kernel(const BwdParams p) {
   };
   auto store_tile = [&](int buf) {
 #pragma unroll
-    for (int u = 0; u < UNITS; ++u) {
-      const int idx = u * 256 + tid;
+    for (int u = 0; u < QUNITS; ++u) {
+      const int idx = u * NT + tid;
       const int row = idx / (D / 8), ch = idx % (D / 8);
-      *reinterpret_cast<bf16x8*>(&Qs[buf][row * NSTR + ch * 8]) = rq[u];
-      *reinterpret_cast<bf16x8*>(&dOs[buf][row * NSTR + ch * 8]) = rd[u];
+      *reinterpret_cast<bf16x8*>(&Qs[buf * QTILE + row * NSTR + ch * 8]) = rq[u];
+      *reinterpret_cast<bf16x8*>(&dOs[buf * QTILE + row * NSTR + ch * 8]) = rd[u];
     }
     if (tid < BM) {
-      lse_s[buf][tid] = lse_r;
-      dvec_s[buf][tid] = dv_r;
+      lse_s[buf * BM + tid] = lse_r;
+      dvec_s[buf * BM + tid] = dv_r;
     }
   };
-  const int tro = tr_lane_ptr(Qs[0], NSTR, 0, 0, lane) - Qs[0];  // transposing-read offset
+  // per-lane LDS offsets: rows of this wave's query half, its key block, and the
+  // transposing reads of the query half
+  const int qrow0 = qh * 32;
+  const int qoff = (qrow0 + c) * NSTR + hh * 8;
+  const int koff = key_loc * NSTR + hh * 8;
+  const int tro = tr_lane_ptr(Qs, NSTR, qrow0, 0, lane) - Qs;
 
   if (n_iter > 0) {
     load_tile(0);
@@ -310,48 +338,42 @@ __global__ __launch_bounds__(256) void dkdv_bf16_kernel(const BwdParams p) {
     const int hg = i / n_vis, j = i - hg * n_vis;
     const int q_rel0 = (qt_first + j) * BM;
     const bool masked = j < n_masked;
-    const bf16* Qb = Qs[buf];
-    const bf16* dOb = dOs[buf];
+    const bf16* Qb = Qs + buf * QTILE;
+    const bf16* dOb = dOs + buf * QTILE;
 
-    f32x16 sacc[2] = {f32x16{}, f32x16{}};
-    f32x16 dpacc[2] = {f32x16{}, f32x16{}};
+    f32x16 sacc = f32x16{}, dpacc = f32x16{};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        const int off = (qb * 32 + c) * NSTR + kk * 16 + hh * 8;
-        bf16x8 a = *reinterpret_cast<const bf16x8*>(&Qb[off]);
-        sacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kf[kk], sacc[qb], 0, 0, 0);
-        bf16x8 b = *reinterpret_cast<const bf16x8*>(&dOb[off]);
-        dpacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, vf[kk], dpacc[qb], 0, 0, 0);
-      }
+      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[koff + kk * 16]);
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Qb[qoff + kk * 16]);
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kf, sacc, 0, 0, 0);
+      const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vs[koff + kk * 16]);
+      const bf16x8 b = *reinterpret_cast<const bf16x8*>(&dOb[qoff + kk * 16]);
+      dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, vf, dpacc, 0, 0, 0);
     }
 
-    bf16x8 pb[4], dsb[4];
-    // lane = key key_loc, rows q = qb*32 + a4*8 + hh*4 + e
-    const int vis_lim = key_rel - diag - q_rel0 - hh * 4;  // visible iff row_local >= vis_lim
+    bf16x8 pb[2], dsb[2];
+    // lane = key key_loc, rows q = qrow0 + a4*8 + hh*4 + e
+    const int vis_lim = key_rel - diag - q_rel0 - hh * 4;  // visible iff row >= vis_lim
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int a4 = 0; a4 < 4; ++a4) {
+      const int ql = qrow0 + a4 * 8 + hh * 4;
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse_s[buf * BM + ql]);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dvec_s[buf * BM + ql]);
 #pragma unroll
-      for (int a4 = 0; a4 < 4; ++a4) {
-        const int ql = qb * 32 + a4 * 8 + hh * 4;
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse_s[buf][ql]);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dvec_s[buf][ql]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = a4 * 4 + e;
-          float pr = fast_exp2(fmaf(sacc[qb][r], p.scale_log2, -l4[e]));
-          if (masked && p.causal) pr = (qb * 32 + a4 * 8 + e) >= vis_lim ? pr : 0.f;
-          pb[qb * 2 + (r >> 3)][r & 7] = f2bf(pr);
-          dsb[qb * 2 + (r >> 3)][r & 7] = f2bf(pr * (dpacc[qb][r] - d4[e]));
-        }
+      for (int e = 0; e < 4; ++e) {
+        const int r = a4 * 4 + e;
+        float pr = fast_exp2(fmaf(sacc[r], p.scale_log2, -l4[e]));
+        if (masked && p.causal) pr = (qrow0 + a4 * 8 + e) >= vis_lim ? pr : 0.f;
+        pb[r >> 3][r & 7] = f2bf(pr);
+        dsb[r >> 3][r & 7] = f2bf(pr * (dpacc[r] - d4[e]));
       }
     }
 
     const bf16* dOt = dOb + tro;
     const bf16* Qt = Qb + tro;
 #pragma unroll
-    for (int qs = 0; qs < 4; ++qs) {
+    for (int qs = 0; qs < 2; ++qs) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         const int off = qs * 16 * NSTR + db * 32;
@@ -369,7 +391,22 @@ __global__ __launch_bounds__(256) void dkdv_bf16_kernel(const BwdParams p) {
     __syncthreads();
   }
 
-  if (kvalid) {
+  // sum the two query halves: waves 4..7 hand their partials to waves 0..3
+  f32x4* red = reinterpret_cast<f32x4*>(smem);  // [kbw][lane][2*DB*16 floats]
+  constexpr int PER_LANE = 2 * DB * 4;           // f32x4 per lane
+  if (qh == 1) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        red[(kbw * 64 + lane) * PER_LANE + db * 4 + a] =
+            f32x4{dvacc[db][a * 4], dvacc[db][a * 4 + 1], dvacc[db][a * 4 + 2], dvacc[db][a * 4 + 3]};
+        red[(kbw * 64 + lane) * PER_LANE + (DB + db) * 4 + a] =
+            f32x4{dkacc[db][a * 4], dkacc[db][a * 4 + 1], dkacc[db][a * 4 + 2], dkacc[db][a * 4 + 3]};
+      }
+  }
+  __syncthreads();
+  if (qh == 0 && key_loc < k_rows) {
     const int64_t row = it.a_start + key_loc;
     bf16* dkp = p.dk + row * kvstride + (int64_t)hk * D + hh * 4;
     bf16* dvp = p.dv + row * kvstride + (int64_t)hk * D + hh * 4;
@@ -377,10 +414,14 @@ __global__ __launch_bounds__(256) void dkdv_bf16_kernel(const BwdParams p) {
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
-        bf16x4 xk = {f2bf(dkacc[db][a * 4 + 0] * p.scale), f2bf(dkacc[db][a * 4 + 1] * p.scale),
-                     f2bf(dkacc[db][a * 4 + 2] * p.scale), f2bf(dkacc[db][a * 4 + 3] * p.scale)};
-        bf16x4 xv = {f2bf(dvacc[db][a * 4 + 0]), f2bf(dvacc[db][a * 4 + 1]),
-                     f2bf(dvacc[db][a * 4 + 2]), f2bf(dvacc[db][a * 4 + 3])};
+        const f32x4 ov = red[(kbw * 64 + lane) * PER_LANE + db * 4 + a];
+        const f32x4 ok = red[(kbw * 64 + lane) * PER_LANE + (DB + db) * 4 + a];
+        bf16x4 xk, xv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          xk[e] = f2bf((dkacc[db][a * 4 + e] + ok[e]) * p.scale);
+          xv[e] = f2bf(dvacc[db][a * 4 + e] + ov[e]);
+        }
         *reinterpret_cast<bf16x4*>(dkp + db * 32 + a * 8) = xk;
         *reinterpret_cast<bf16x4*>(dvp + db * 32 + a * 8) = xv;
       }
@@ -438,9 +479,9 @@ hipError_t launch_dkdv_bf16(const bs_dims& dims, const void* q, const void* k, c
   p.dv = static_cast<bf16*>(dv);
   const dim3 grid((unsigned)(L.max_items * dims.hkv));
   if (dims.head_dim == 128)
-    hipLaunchKernelGGL(dkdv_bf16_kernel<128>, grid, dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(dkdv_bf16_kernel<128>, grid, dim3(512), 0, stream, p);
   else
-    hipLaunchKernelGGL(dkdv_bf16_kernel<64>, grid, dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(dkdv_bf16_kernel<64>, grid, dim3(512), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -184,6 +184,104 @@ def cpu_baseline_varlen(W, scale):
             "seconds": dt}
 
 
+def chunk_workload(name):
+    """(hq, hkv, chunk tokens, Q part offsets, KV part offsets, (q, kv) pairs) of a CP share."""
+    c = 32768
+    if name == "cp7b":
+        # one 32K Q chunk at 1015808 (the last of a 2048K sequence's 31st..32nd positions) against
+        # 8 KV chunks, the 7 before it and its own (diagonal)
+        q_offs = [1015808]
+        kv_offs = [(24 + i) * c for i in range(8)]
+        return 32, 32, c, q_offs, kv_offs, [(0, j) for j in range(8)]
+    # device 0 of a 4-way symmetric split of a 256K sequence into 8 parts: parts 0 and 7
+    q_offs = [0, 7 * c]
+    kv_offs = [0, 7 * c]
+    return 48, 8, c, q_offs, kv_offs, [(i, j) for i in range(2) for j in range(2)]
+
+
+def run_chunk_bench(args, dev):
+    import torch
+    from paper_2502_21231_amd import bs_attn as B
+    from paper_2502_21231_amd import inputs
+    hq, hkv, c, q_offs, kv_offs, pairs = chunk_workload(args.workload)
+    d, seed = 128, args.seed
+    scale = 1.0 / math.sqrt(d)
+    Q = [inputs.normal(seed, inputs.TID_Q + 100 * i, (c, hq, d)).to(dev) for i in range(len(q_offs))]
+    dO = [inputs.normal(seed, inputs.TID_DO + 100 * i, (c, hq, d)).to(dev) for i in range(len(q_offs))]
+    K = [inputs.normal(seed, inputs.tid_chunk_k(j), (c, hkv, d)).to(dev) for j in range(len(kv_offs))]
+    V = [inputs.normal(seed, inputs.tid_chunk_v(j), (c, hkv, d)).to(dev) for j in range(len(kv_offs))]
+    dims = B.make_dims(Q[0], K[0])
+    ws_f = B.alloc_workspace(B.BS_OP_CHUNK_FWD, dims, dev)
+    ws_b = B.alloc_workspace(B.BS_OP_CHUNK_BWD, dims, dev)
+    per_q = {i: [j for (a, j) in pairs if a == i] for i in range(len(q_offs))}
+    per_kv = {j: [i for (i, b) in pairs if b == j] for j in range(len(kv_offs))}
+    parts_o = {i: torch.empty(len(per_q[i]), c, hq, d, dtype=torch.bfloat16, device=dev) for i in per_q}
+    parts_l = {i: torch.empty(len(per_q[i]), hq, c, dtype=torch.float32, device=dev) for i in per_q}
+    O = [torch.empty(c, hq, d, dtype=torch.bfloat16, device=dev) for _ in q_offs]
+    L = [torch.empty(hq, c, dtype=torch.float32, device=dev) for _ in q_offs]
+    dq_acc = [torch.empty(c, hq, d, dtype=torch.float32, device=dev) for _ in q_offs]
+    dQ = [torch.empty(c, hq, d, dtype=torch.bfloat16, device=dev) for _ in q_offs]
+    multi = any(len(v) > 1 for v in per_kv.values())   # a KV part seen by several Q parts
+    kv_dtype = torch.float32 if multi else torch.bfloat16
+    dK = [torch.empty(c, hkv, d, dtype=kv_dtype, device=dev) for _ in kv_offs]
+    dV = [torch.empty(c, hkv, d, dtype=kv_dtype, device=dev) for _ in kv_offs]
+    dKb = [torch.empty(c, hkv, d, dtype=torch.bfloat16, device=dev) for _ in kv_offs] if multi else dK
+    dVb = [torch.empty(c, hkv, d, dtype=torch.bfloat16, device=dev) for _ in kv_offs] if multi else dV
+
+    def step():
+        for i in per_q:
+            for s, j in enumerate(per_q[i]):
+                B.bs_attn_chunk_fwd(Q[i], K[j], V[j], q_offs[i], kv_offs[j], True, scale,
+                                    parts_o[i][s], parts_l[i][s], ws_f)
+            B.bs_lse_merge(parts_o[i], parts_l[i], O[i], L[i])
+        for t in dq_acc:
+            t.zero_()
+        if multi:
+            for t in dK + dV:
+                t.zero_()
+        for i, j in pairs:
+            B.bs_attn_chunk_bwd(Q[i], K[j], V[j], O[i], L[i], dO[i], q_offs[i], kv_offs[j], True,
+                                scale, dq_acc[i], dK[j], dV[j], multi, ws_b)
+        for i in range(len(q_offs)):
+            B.bs_dq_finalize(dq_acc[i], dQ[i])
+        if multi:
+            for j in range(len(kv_offs)):
+                B.bs_dq_finalize(dK[j], dKb[j])
+                B.bs_dq_finalize(dV[j], dVb[j])
+
+    A = sum(visible_pairs_chunk_closed(c, c, q_offs[i] - kv_offs[j]) for i, j in pairs)
+    flops_fwd = 4 * d * hq * A
+    flops_bwd = 10 * d * hq * A
+    res = time_steps(step, args, dev, flops_fwd, flops_bwd)
+    res["config"] = {"workload": WORKLOADS[args.workload], "chunk_tokens": c, "heads_q": hq,
+                     "heads_kv": hkv, "head_dim": d, "q_offsets": q_offs, "kv_offsets": kv_offs,
+                     "pairs": pairs, "seed": seed, "visible_pairs": A}
+    res["flops_per_step"] = flops_fwd + flops_bwd
+    merge = res["kernels"].get("lse_merge")
+    if merge:
+        # algorithmic bytes of one merge of n partials: read n O and LSE rows, write one of each
+        n = len(per_q[0])
+        nbytes = n * c * hq * d * 2 + n * hq * c * 4 + c * hq * d * 2 + hq * c * 4
+        res["lse_merge_gbs"] = nbytes / (merge["avg_ms_per_launch"] * 1e-3) / 1e9
+    return res
+
+
+def visible_pairs_chunk_closed(lq, lk, diag):
+    """Exact visible (query, key) pairs of a chunk pair: key j visible to query i iff j - i <= diag."""
+    tot = 0
+    # rows i with i + diag + 1 in (0, lk): a triangle; rows beyond see every key
+    lo = max(0, -diag)                  # first row that sees key 0
+    hi = min(lq, lk - diag - 1)         # rows below hi see fewer than lk keys
+    if hi > lo:
+        n = hi - lo
+        first = lo + diag + 1
+        tot += n * first + n * (n - 1) // 2
+    full_from = max(lo, hi, 0)
+    if lq > full_from:
+        tot += (lq - full_from) * lk
+    return tot
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -218,7 +316,7 @@ def main():
     if args.workload in ("packed7b", "gqa70b"):
         res = run_varlen_bench(args, dev)
     else:
-        raise SystemExit(f"workload {args.workload} is not implemented yet")
+        res = run_chunk_bench(args, dev)
     line = {
         "metric": "attention fwd+bwd TFLOP/s (causal-adjusted) and % of bf16 MFMA peak, 1 GPU",
         "value": round(res["value"], 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
@@ -229,6 +327,7 @@ def main():
         "fwd_tflops": res["fwd_tflops"], "bwd_tflops": res["bwd_tflops"],
         "kernels": res["kernels"], "flops_per_step": res["flops_per_step"],
         "roofline": res["roofline"],
+        "lse_merge_gbs": res.get("lse_merge_gbs"),
         "cpu_baseline": res.get("cpu_baseline"),
     }
     print(json.dumps(line), flush=True)

@@ -140,14 +140,17 @@ int bs_attn_chunk_fwd(const bs_dims* dims, const void* q, const void* k, const v
 
 /* Backward of one context-parallel step.  out_merged / lse_merged are the
  * final (merged over all steps) forward results.  Adds this step's dQ
- * contribution, multiplied by nothing else, into dq_accum (float32
- * [T, hq, d], caller-zeroed before the first step), and writes this KV
- * shard's dk, dv [Tk, hkv, d].  After the last step, bs_dq_finalize()
- * rounds dq_accum into dq. */
+ * contribution into dq_accum (float32 [T, hq, d], caller-zeroed before the
+ * first step).  This KV shard's dK, dV [Tk, hkv, d]: with kv_accumulate == 0,
+ * dk and dv are outputs of dims->dtype, overwritten; with kv_accumulate != 0
+ * they are float32 accumulators (caller-zeroed) to which this step's
+ * contribution is added, for a KV shard that several Q shards attend to (the
+ * symmetric 2N-way split of Sec. 7, Dist-attn with packing).  bs_dq_finalize()
+ * rounds any such float32 accumulator into dims->dtype. */
 int bs_attn_chunk_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,
                       const void* out_merged, const float* lse_merged, const void* dout,
                       int64_t q_pos_offset, int64_t k_pos_offset, int causal, float scale,
-                      float* dq_accum, void* dk, void* dv, void* workspace,
+                      float* dq_accum, void* dk, void* dv, int kv_accumulate, void* workspace,
                       size_t workspace_bytes, void* stream);
 
 /* Rounds a float32 dQ accumulator [T, hq, d] into dq of dims->dtype (RNE). */

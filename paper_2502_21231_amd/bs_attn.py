@@ -64,7 +64,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "bs_attn_chunk_fwd": (ctypes.c_int, [_DIMS, _P, _P, _P, _I64, _I64, ctypes.c_int, _F, _P, _P,
                                              _P, _SZ, _P]),
         "bs_attn_chunk_bwd": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _I64, _I64, ctypes.c_int,
-                                             _F, _P, _P, _P, _P, _SZ, _P]),
+                                             _F, _P, _P, _P, ctypes.c_int, _P, _SZ, _P]),
         "bs_dq_finalize": (ctypes.c_int, [_DIMS, _P, _P, _P]),
         "bs_lse_merge": (ctypes.c_int, [_DIMS, _P, _P, _I32, _P, _P, _P]),
         "bs_read_device_status": (ctypes.c_int, [_P, _P]),
@@ -223,9 +223,10 @@ def bs_attn_chunk_fwd(q, k, v, q_pos_offset: int, k_pos_offset: int, causal: boo
 
 def bs_attn_chunk_bwd(q, k, v, out_merged, lse_merged, dout, q_pos_offset: int, k_pos_offset: int,
                       causal: bool = True, scale: float | None = None, dq_accum=None, dk=None,
-                      dv=None, workspace=None):
+                      dv=None, kv_accumulate: bool = False, workspace=None):
     """Backward of one context-parallel step: adds into dq_accum (float32, caller-zeroed) and
-    returns (dq_accum, dk, dv) of this KV shard."""
+    returns (dq_accum, dk, dv) of this KV shard.  With kv_accumulate, dk and dv are float32
+    accumulators (caller-zeroed) that this step's contribution is added to."""
     _qkv(q, k, v)
     _need(out_merged, "out_merged", q.dtype)
     _need(dout, "dout", q.dtype)
@@ -234,15 +235,20 @@ def bs_attn_chunk_bwd(q, k, v, out_merged, lse_merged, dout, q_pos_offset: int, 
     if dq_accum is None:
         dq_accum = torch.zeros(q.shape, dtype=torch.float32, device=q.device)
     _need(dq_accum, "dq_accum", torch.float32)
-    dk = torch.empty_like(k) if dk is None else dk
-    dv = torch.empty_like(v) if dv is None else dv
+    kv_dtype = torch.float32 if kv_accumulate else k.dtype
+    if dk is None:
+        dk = torch.zeros(k.shape, dtype=kv_dtype, device=k.device)
+    if dv is None:
+        dv = torch.zeros(v.shape, dtype=kv_dtype, device=v.device)
+    _need(dk, "dk", kv_dtype)
+    _need(dv, "dv", kv_dtype)
     if workspace is None:
         workspace = alloc_workspace(BS_OP_CHUNK_BWD, dims, q.device)
     _check(load_library().bs_attn_chunk_bwd(
         ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(out_merged), _ptr(lse_merged),
         _ptr(dout), int(q_pos_offset), int(k_pos_offset), int(bool(causal)),
-        _scale(scale, q.shape[2]), _ptr(dq_accum), _ptr(dk), _ptr(dv), _ptr(workspace),
-        workspace.numel(), _stream(q.device)))
+        _scale(scale, q.shape[2]), _ptr(dq_accum), _ptr(dk), _ptr(dv), int(bool(kv_accumulate)),
+        _ptr(workspace), workspace.numel(), _stream(q.device)))
     return dq_accum, dk, dv
 
 

@@ -47,6 +47,8 @@ struct BwdParams {
   float* dq_acc;     // chunk: dQ added into a float32 accumulator (dq == nullptr)
   bf16* dk;
   bf16* dv;
+  float* dk_acc;     // when set, dK and dV are added into float32 accumulators
+  float* dv_acc;
   const WsHeader* hdr;
   const WorkItem* items;
   int64_t total_q;
@@ -407,23 +409,31 @@ void dkdv_bf16_kernel(const BwdParams p) {
   }
   __syncthreads();
   if (qh == 0 && key_loc < k_rows) {
-    const int64_t row = it.a_start + key_loc;
-    bf16* dkp = p.dk + row * kvstride + (int64_t)hk * D + hh * 4;
-    bf16* dvp = p.dv + row * kvstride + (int64_t)hk * D + hh * 4;
+    const int64_t off = (int64_t)(it.a_start + key_loc) * kvstride + (int64_t)hk * D + hh * 4;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
         const f32x4 ov = red[(kbw * 64 + lane) * PER_LANE + db * 4 + a];
         const f32x4 ok = red[(kbw * 64 + lane) * PER_LANE + (DB + db) * 4 + a];
-        bf16x4 xk, xv;
+        f32x4 gk, gv;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          xk[e] = f2bf((dkacc[db][a * 4 + e] + ok[e]) * p.scale);
-          xv[e] = f2bf(dvacc[db][a * 4 + e] + ov[e]);
+          gk[e] = (dkacc[db][a * 4 + e] + ok[e]) * p.scale;
+          gv[e] = dvacc[db][a * 4 + e] + ov[e];
         }
-        *reinterpret_cast<bf16x4*>(dkp + db * 32 + a * 8) = xk;
-        *reinterpret_cast<bf16x4*>(dvp + db * 32 + a * 8) = xv;
+        const int col = db * 32 + a * 8;
+        if (p.dk_acc != nullptr) {  // add into float32 accumulators
+          f32x4* dk4 = reinterpret_cast<f32x4*>(p.dk_acc + off + col);
+          f32x4* dv4 = reinterpret_cast<f32x4*>(p.dv_acc + off + col);
+          *dk4 = *dk4 + gk;
+          *dv4 = *dv4 + gv;
+        } else {
+          const bf16x4 xk = {f2bf(gk[0]), f2bf(gk[1]), f2bf(gk[2]), f2bf(gk[3])};
+          const bf16x4 xv = {f2bf(gv[0]), f2bf(gv[1]), f2bf(gv[2]), f2bf(gv[3])};
+          *reinterpret_cast<bf16x4*>(p.dk + off + col) = xk;
+          *reinterpret_cast<bf16x4*>(p.dv + off + col) = xv;
+        }
       }
     }
   }
@@ -471,12 +481,17 @@ hipError_t launch_dq_bf16(const bs_dims& dims, const void* q, const void* k, con
 
 hipError_t launch_dkdv_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
                             const void* dout, const float* lse, const float* dvec, int causal,
-                            float scale, void* dk, void* dv, const void* ws, const WsLayout& L,
-                            hipStream_t stream) {
+                            float scale, void* dk, void* dv, int kv_accumulate, const void* ws,
+                            const WsLayout& L, hipStream_t stream) {
   if (L.max_items == 0 || dims.hkv == 0) return hipSuccess;
   BwdParams p = make_params(dims, q, k, v, dout, lse, dvec, causal, scale, ws, L);
-  p.dk = static_cast<bf16*>(dk);
-  p.dv = static_cast<bf16*>(dv);
+  if (kv_accumulate) {
+    p.dk_acc = static_cast<float*>(dk);
+    p.dv_acc = static_cast<float*>(dv);
+  } else {
+    p.dk = static_cast<bf16*>(dk);
+    p.dv = static_cast<bf16*>(dv);
+  }
   const dim3 grid((unsigned)(L.max_items * dims.hkv));
   if (dims.head_dim == 128)
     hipLaunchKernelGGL(dkdv_bf16_kernel<128>, grid, dim3(512), 0, stream, p);

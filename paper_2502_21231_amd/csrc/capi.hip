@@ -251,7 +251,7 @@ int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
                const void* out, const float* lse, const void* dout, const int32_t* cu_q,
                const int32_t* cu_k, int32_t num_seqs, int32_t max_seqlen, int64_t q_off,
                int64_t k_off, int causal, float scale, float* dq_accum, void* dq, void* dk,
-               void* dv, void* ws, size_t ws_bytes, void* stream) {
+               void* dv, int kv_accumulate, void* ws, size_t ws_bytes, void* stream) {
   BS_TRY(check_dims(dims, true));
   const bs_dims& d = *dims;
   const int64_t qn = d.total_q * d.hq * d.head_dim, kn = d.total_k * d.hkv * d.head_dim;
@@ -304,10 +304,12 @@ int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
   {
     ProfScope ps(BS_KERNEL_BWD_DKDV, s);
     if (f32)
-      BS_HIP(launch_bwd_f32_dkdv(d, q, k, v, lse, dout, dvec, causal, scale, dk, dv, ws, Lp, s),
+      BS_HIP(launch_bwd_f32_dkdv(d, q, k, v, lse, dout, dvec, causal, scale, dk, dv, kv_accumulate,
+                                 ws, Lp, s),
              "backward dK/dV launch");
     else
-      BS_HIP(launch_dkdv_bf16(d, q, k, v, dout, lse, dvec, causal, scale, dk, dv, ws, Lp, s),
+      BS_HIP(launch_dkdv_bf16(d, q, k, v, dout, lse, dvec, causal, scale, dk, dv, kv_accumulate,
+                              ws, Lp, s),
              "backward dK/dV launch");
   }
   if (varlen && f32) {
@@ -352,7 +354,7 @@ int bs_attn_varlen_bwd(const bs_dims* dims, const void* q, const void* k, const 
                        int32_t max_seqlen, int causal, float scale, void* dq, void* dk, void* dv,
                        void* workspace, size_t workspace_bytes, void* stream) {
   return bwd_common(BS_OP_VARLEN_BWD, dims, q, k, v, out, lse, dout, cu_seqlens_q, cu_seqlens_k,
-                    num_seqs, max_seqlen, 0, 0, causal, scale, nullptr, dq, dk, dv, workspace,
+                    num_seqs, max_seqlen, 0, 0, causal, scale, nullptr, dq, dk, dv, 0, workspace,
                     workspace_bytes, stream);
 }
 
@@ -367,11 +369,11 @@ int bs_attn_chunk_fwd(const bs_dims* dims, const void* q, const void* k, const v
 int bs_attn_chunk_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,
                       const void* out_merged, const float* lse_merged, const void* dout,
                       int64_t q_pos_offset, int64_t k_pos_offset, int causal, float scale,
-                      float* dq_accum, void* dk, void* dv, void* workspace,
+                      float* dq_accum, void* dk, void* dv, int kv_accumulate, void* workspace,
                       size_t workspace_bytes, void* stream) {
   return bwd_common(BS_OP_CHUNK_BWD, dims, q, k, v, out_merged, lse_merged, dout, nullptr, nullptr,
                     1, 0, q_pos_offset, k_pos_offset, causal, scale, dq_accum, nullptr, dk, dv,
-                    workspace, workspace_bytes, stream);
+                    kv_accumulate != 0, workspace, workspace_bytes, stream);
 }
 
 int bs_dq_finalize(const bs_dims* dims, const float* dq_accum, void* dq, void* stream) {

@@ -122,8 +122,8 @@ hipError_t launch_dq_bf16(const bs_dims& dims, const void* q, const void* k, con
                           hipStream_t stream);
 hipError_t launch_dkdv_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
                             const void* dout, const float* lse, const float* dvec, int causal,
-                            float scale, void* dk, void* dv, const void* ws, const WsLayout& L,
-                            hipStream_t stream);
+                            float scale, void* dk, void* dv, int kv_accumulate, const void* ws,
+                            const WsLayout& L, hipStream_t stream);
 
 hipError_t launch_fwd_f32(const bs_dims& dims, const void* q, const void* k, const void* v,
                           int causal, float scale, void* out, float* lse, const void* ws,
@@ -134,8 +134,8 @@ hipError_t launch_bwd_f32_dq(const bs_dims& dims, const void* q, const void* k, 
                              hipStream_t stream);
 hipError_t launch_bwd_f32_dkdv(const bs_dims& dims, const void* q, const void* k, const void* v,
                                const float* lse, const void* dout, const float* dvec, int causal,
-                               float scale, void* dk, void* dv, const void* ws,
-                               const WsLayout& L, hipStream_t stream);
+                               float scale, void* dk, void* dv, int kv_accumulate,
+                               const void* ws, const WsLayout& L, hipStream_t stream);
 
 hipError_t launch_bwd_preprocess(const bs_dims& dims, const void* out, const void* dout,
                                  float* dvec, float* dq_acc_to_zero, const void* ws,

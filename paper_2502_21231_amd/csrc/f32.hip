@@ -28,6 +28,7 @@ struct F32Params {
   int64_t total_q;
   int32_t hq, hkv, group;
   int32_t causal;
+  int32_t kv_accumulate;  // dK, dV added into (not written over) the outputs
   float scale, scale_log2;
 };
 
@@ -227,10 +228,12 @@ __global__ __launch_bounds__(BN) void bwd_dkdv_f32_kernel(const F32Params p) {
     }
   }
   if (valid) {
+    float* dkp = p.dk + row * ks + (int64_t)hk * D;
+    float* dvp = p.dv + row * ks + (int64_t)hk * D;
 #pragma unroll
     for (int i = 0; i < D; ++i) {
-      p.dk[row * ks + (int64_t)hk * D + i] = dka[i] * p.scale;
-      p.dv[row * ks + (int64_t)hk * D + i] = dva[i];
+      dkp[i] = (p.kv_accumulate ? dkp[i] : 0.f) + dka[i] * p.scale;
+      dvp[i] = (p.kv_accumulate ? dvp[i] : 0.f) + dva[i];
     }
   }
 }
@@ -289,10 +292,11 @@ hipError_t launch_bwd_f32_dq(const bs_dims& dims, const void* q, const void* k, 
 
 hipError_t launch_bwd_f32_dkdv(const bs_dims& dims, const void* q, const void* k, const void* v,
                                const float* lse, const void* dout, const float* dvec, int causal,
-                               float scale, void* dk, void* dv, const void* ws,
-                               const WsLayout& L, hipStream_t stream) {
+                               float scale, void* dk, void* dv, int kv_accumulate,
+                               const void* ws, const WsLayout& L, hipStream_t stream) {
   if (L.max_items == 0 || dims.hkv == 0) return hipSuccess;
   F32Params p = make_params(dims, ws, L, causal, scale);
+  p.kv_accumulate = kv_accumulate;
   p.q = static_cast<const float*>(q);
   p.k = static_cast<const float*>(k);
   p.v = static_cast<const float*>(v);

@@ -1,0 +1,201 @@
+"""GPU parity at the full workload sizes, through the same C-ABI calls the benchmark times.
+
+The oracle cannot redo a whole 32K..131K-token problem in seconds, so it checks
+  * sampled query rows one by one (O, LSE, dQ): a row needs only its own keys;
+  * sampled keys near the end of a segment or diagonal chunk (dK, dV): only the few
+    query rows after them see them, so the oracle needs only those rows;
+and every output is checked against properties that hold at any size: per segment
+(or per query shard) and KV head, sum_j dK_j = 0 and sum_j dV_j = sum over the group's
+query heads of sum_i dO_i (the rows of P sum to 1, the rows of dS to 0).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as A
+from paper_2502_21231_amd import bs_attn as B
+from paper_2502_21231_amd import inputs
+from tests.parity_util import check_close, check_lse, f64
+
+pytestmark = pytest.mark.gpu
+BF = torch.bfloat16
+D = 128
+SCALE = 1.0 / math.sqrt(D)
+
+
+def gen(seed, tid, shape):
+    return inputs.normal(seed, tid, shape, BF)
+
+
+def row_oracle(qrow, K, V, dorow, q_pos, k_pos):
+    """O, LSE, dQ of single query rows [1, G, d] against one key range [L, 1, d]."""
+    o, l = A.chunk_fwd(qrow, K, V, q_pos, k_pos, True, SCALE)
+    o_in = torch.from_numpy(o).to(BF)
+    dq, _, _ = A.chunk_bwd(qrow, K, V, o_in, l, dorow, q_pos, k_pos, True, SCALE)
+    return o, l, dq
+
+
+def check_grad_sums(name, dk, dv, do, hq, hkv, key_ranges, row_ranges):
+    """sum dK = 0 and sum dV = sum dO over each (key range, row range) group, every KV head."""
+    G = hq // hkv
+    for (k0, k1), (r0, r1) in zip(key_ranges, row_ranges):
+        sk = dk[k0:k1].double().sum(dim=0)           # [hkv, d]
+        sv = dv[k0:k1].double().sum(dim=0)
+        so = do[r0:r1].double().sum(dim=0).reshape(hkv, G, D).sum(dim=1)
+        n = (k1 - k0) * G
+        tol = 0.02 * math.sqrt(max(n, 1)) + 1e-3 * float(so.abs().max())
+        assert float(sk.abs().max()) <= tol, (name, "sum dK", float(sk.abs().max()), tol)
+        assert float((sv - so).abs().max()) <= tol, (name, "sum dV", float((sv - so).abs().max()), tol)
+
+
+def varlen_fullsize(lens, hq, hkv, seed):
+    T = sum(lens)
+    G = hq // hkv
+    cu = inputs.cu_seqlens(lens)
+    q = gen(seed, inputs.TID_Q, (T, hq, D))
+    k = gen(seed, inputs.TID_K, (T, hkv, D))
+    v = gen(seed, inputs.TID_V, (T, hkv, D))
+    do = gen(seed, inputs.TID_DO, (T, hq, D))
+    cug = torch.from_numpy(cu).cuda()
+    qg, kg, vg, dog = q.cuda(), k.cuda(), v.cuda(), do.cuda()
+    maxlen = max(lens)
+    out, lse = B.bs_attn_varlen_fwd(qg, kg, vg, cug, cug, maxlen, True, SCALE)
+    dq, dk, dv = B.bs_attn_varlen_bwd(qg, kg, vg, out, lse, dog, cug, cug, maxlen, True, SCALE)
+    torch.cuda.synchronize()
+    out_c, lse_c, dq_c, dk_c, dv_c = (t.cpu() for t in (out, lse, dq, dk, dv))
+    assert torch.isfinite(out_c.float()).all() and torch.isfinite(dq_c.float()).all()
+    assert torch.isfinite(dk_c.float()).all() and torch.isfinite(dv_c.float()).all()
+
+    rng = np.random.default_rng(seed + 1000)
+    heads = sorted({0, hq - 1, int(rng.integers(0, hq))})
+    order = np.argsort(lens)[::-1]
+    segs = list(order[:2]) + list(order[-2:]) + [int(rng.integers(0, len(lens)))]
+    for b in sorted(set(int(x) for x in segs)):
+        s, L = int(cu[b]), lens[b]
+        rows = sorted({0, L - 1, L // 2, int(rng.integers(0, L)), min(L - 1, 127), min(L - 1, 128)})
+        for h in heads:
+            hk = h // G
+            K, V = k[s:s + L, hk:hk + 1], v[s:s + L, hk:hk + 1]
+            for i in rows:
+                o, l, g = row_oracle(q[s + i:s + i + 1, h:h + 1], K, V, do[s + i:s + i + 1, h:h + 1], i, 0)
+                check_close(f"O seg{b} row{i} h{h}", f64(out_c[s + i, h]), o[0, 0], 2e-2, True)
+                check_lse(f"LSE seg{b} row{i} h{h}", f64(lse_c[h, s + i:s + i + 1]), l[0], 1e-3)
+                check_close(f"dQ seg{b} row{i} h{h}", f64(dq_c[s + i, h]), g[0, 0], 2e-2, True)
+    # dK, dV of the last 48 keys of the two longest segments, KV head 0 and the last one
+    for b in [int(x) for x in order[:2]]:
+        s, L = int(cu[b]), lens[b]
+        r0 = max(0, L - 48)
+        for hk in sorted({0, hkv - 1}):
+            hs = slice(hk * G, (hk + 1) * G)
+            qb, dob = q[s + r0:s + L, hs], do[s + r0:s + L, hs]
+            K, V = k[s:s + L, hk:hk + 1], v[s:s + L, hk:hk + 1]
+            o, l = A.chunk_fwd(qb, K, V, r0, 0, True, SCALE)
+            _, gk, gv = A.chunk_bwd(qb, K, V, torch.from_numpy(o).to(BF), l, dob, r0, 0, True, SCALE)
+            check_close(f"dK seg{b} hk{hk}", f64(dk_c[s + r0:s + L, hk:hk + 1]), gk[r0:], 2e-2, True)
+            check_close(f"dV seg{b} hk{hk}", f64(dv_c[s + r0:s + L, hk:hk + 1]), gv[r0:], 2e-2, True)
+    ranges = [(int(cu[b]), int(cu[b + 1])) for b in range(len(lens))]
+    check_grad_sums("varlen", dk_c, dv_c, do, hq, hkv, ranges, ranges)
+
+
+def test_packed_7b_32k_lognormal_seed0(gpu):
+    """32768 tokens, 32/32 heads, log-normal lengths (seed 0): the benchmark workload."""
+    varlen_fullsize(inputs.lognormal_packed_lengths(0), 32, 32, 0)
+
+
+def test_gqa_70b_131k_mixed_seed0(gpu):
+    """131072 tokens, 64/8 heads, one 60642-token segment among 33 shorts."""
+    varlen_fullsize(inputs.mixed_long_short_lengths(0), 64, 8, 0)
+
+
+def chunk_share(hq, hkv, q_offs, kv_offs, pairs, seed, c=32768):
+    """A context-parallel share: per-step chunk forward, LSE merge, per-step chunk backward with
+    dQ (and, for KV parts seen by several Q parts, dK/dV) accumulated in float32."""
+    G = hq // hkv
+    Q = [gen(seed, inputs.TID_Q + 100 * i, (c, hq, D)) for i in range(len(q_offs))]
+    dO = [gen(seed, inputs.TID_DO + 100 * i, (c, hq, D)) for i in range(len(q_offs))]
+    K = [gen(seed, inputs.tid_chunk_k(j), (c, hkv, D)) for j in range(len(kv_offs))]
+    V = [gen(seed, inputs.tid_chunk_v(j), (c, hkv, D)) for j in range(len(kv_offs))]
+    Qg, dOg = [t.cuda() for t in Q], [t.cuda() for t in dO]
+    Kg, Vg = [t.cuda() for t in K], [t.cuda() for t in V]
+    per_q = {i: [j for (a, j) in pairs if a == i] for i in range(len(q_offs))}
+    multi = any(sum(1 for (_, b) in pairs if b == j) > 1 for j in range(len(kv_offs)))
+    O, L = [], []
+    for i in range(len(q_offs)):
+        po, pl = zip(*[B.bs_attn_chunk_fwd(Qg[i], Kg[j], Vg[j], q_offs[i], kv_offs[j], True, SCALE)
+                       for j in per_q[i]])
+        o, l = B.bs_lse_merge(torch.stack(po), torch.stack(pl))
+        O.append(o)
+        L.append(l)
+    acc = [torch.zeros(c, hq, D, dtype=torch.float32, device="cuda") for _ in q_offs]
+    kvt = torch.float32 if multi else BF
+    dK = [torch.zeros(c, hkv, D, dtype=kvt, device="cuda") for _ in kv_offs]
+    dV = [torch.zeros(c, hkv, D, dtype=kvt, device="cuda") for _ in kv_offs]
+    for i, j in pairs:
+        B.bs_attn_chunk_bwd(Qg[i], Kg[j], Vg[j], O[i], L[i], dOg[i], q_offs[i], kv_offs[j], True,
+                            SCALE, acc[i], dK[j], dV[j], multi)
+    dQ = [B.bs_dq_finalize(a, torch.empty(c, hq, D, dtype=BF, device="cuda")) for a in acc]
+    if multi:
+        dK = [B.bs_dq_finalize(t, torch.empty(c, hkv, D, dtype=BF, device="cuda")) for t in dK]
+        dV = [B.bs_dq_finalize(t, torch.empty(c, hkv, D, dtype=BF, device="cuda")) for t in dV]
+    torch.cuda.synchronize()
+    O, L, dQ, dK, dV = ([t.cpu() for t in x] for x in (O, L, dQ, dK, dV))
+
+    rng = np.random.default_rng(seed + 2000)
+    heads = sorted({0, hq - 1, int(rng.integers(0, hq))})
+    for i in range(len(q_offs)):
+        rows = sorted({0, 1, c - 1, c // 2, int(rng.integers(0, c))})
+        for h in heads:
+            hk = h // G
+            for r in rows:
+                outs = [A.chunk_fwd(Q[i][r:r + 1, h:h + 1], K[j][:, hk:hk + 1], V[j][:, hk:hk + 1],
+                                    q_offs[i] + r, kv_offs[j], True, SCALE) for j in per_q[i]]
+                o, l = A.lse_merge(np.stack([x[0] for x in outs]), np.stack([x[1] for x in outs]))
+                check_close(f"O q{i} row{r} h{h}", f64(O[i][r, h]), o[0, 0], 2e-2, True)
+                check_lse(f"LSE q{i} row{r} h{h}", f64(L[i][h, r:r + 1]), l[0], 1e-3)
+                o_in = torch.from_numpy(o).to(BF)
+                g = sum(A.chunk_bwd(Q[i][r:r + 1, h:h + 1], K[j][:, hk:hk + 1], V[j][:, hk:hk + 1],
+                                    o_in, l, dO[i][r:r + 1, h:h + 1], q_offs[i] + r, kv_offs[j], True,
+                                    SCALE)[0] for j in per_q[i])
+                check_close(f"dQ q{i} row{r} h{h}", f64(dQ[i][r, h]), g[0, 0], 2e-2, True)
+    # dK, dV of the last 48 keys of each KV part that no later Q part attends to: only the
+    # last 48 rows of its diagonal Q part see them (earlier Q parts see none of it)
+    for j, kv0 in enumerate(kv_offs):
+        seers = [i for (i, b) in pairs if b == j]
+        if any(q_offs[i] > kv0 for i in seers):
+            continue  # a later Q part sees every key of it: covered by the sums below
+        for hk in sorted({0, hkv - 1}):
+            hs = slice(hk * G, (hk + 1) * G)
+            for i in seers:
+                if q_offs[i] != kv0:
+                    continue
+                r0 = c - 48
+                qb, dob = Q[i][r0:, hs], dO[i][r0:, hs]
+                outs = [A.chunk_fwd(qb, K[jj][:, hk:hk + 1], V[jj][:, hk:hk + 1], q_offs[i] + r0,
+                                    kv_offs[jj], True, SCALE) for jj in per_q[i]]
+                o, l = A.lse_merge(np.stack([x[0] for x in outs]), np.stack([x[1] for x in outs]))
+                _, gk, gv = A.chunk_bwd(qb, K[j][:, hk:hk + 1], V[j][:, hk:hk + 1],
+                                        torch.from_numpy(o).to(BF), l, dob, q_offs[i] + r0, kv0, True,
+                                        SCALE)
+                check_close(f"dK kv{j} hk{hk}", f64(dK[j][r0:, hk:hk + 1]), gk[r0:], 2e-2, True)
+                check_close(f"dV kv{j} hk{hk}", f64(dV[j][r0:, hk:hk + 1]), gv[r0:], 2e-2, True)
+    # every key of the share: each Q row's visible keys all lie in the share's KV parts, so the
+    # sums over all KV parts match the sums over all Q parts
+    dk_all = torch.cat(dK)
+    dv_all = torch.cat(dV)
+    do_all = torch.cat(dO)
+    check_grad_sums("cp share", dk_all, dv_all, do_all, hq, hkv, [(0, dk_all.shape[0])],
+                    [(0, do_all.shape[0])])
+
+
+def test_cp_share_7b_2048k(gpu):
+    """A 32768-token Q chunk at 1015808 against 8 KV chunks at (24..31)*32768, 32/32 heads."""
+    c = 32768
+    chunk_share(32, 32, [1015808], [(24 + i) * c for i in range(8)], [(0, j) for j in range(8)], 0)
+
+
+def test_zigzag_share_141b_256k(gpu):
+    """Device 0 of a 4-way symmetric split: Q/KV parts 0 and 7 of a 256K sequence, 48/8 heads."""
+    c = 32768
+    chunk_share(48, 8, [0, 7 * c], [0, 7 * c], [(i, j) for i in range(2) for j in range(2)], 0)

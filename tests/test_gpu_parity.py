@@ -168,6 +168,48 @@ def test_cp_ring_share_fwd_merge_bwd(gpu):
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_chunk_bwd_accumulates_kv_over_q_parts(gpu, dtype):
+    """Symmetric 2-part split: Q parts 0 and 3 (of 4) against KV parts 0 and 3; dK/dV of each KV
+    part summed over both Q parts in float32 accumulators, then rounded by bs_dq_finalize."""
+    c, hq, hkv, d = 96, 4, 2, 64
+    offs = [0, 3 * c]
+    Q = [inputs.normal(15, 100 * i, (c, hq, d), dtype) for i in range(2)]
+    dO = [inputs.normal(15, 3 + 100 * i, (c, hq, d), dtype) for i in range(2)]
+    K = [inputs.normal(15, inputs.tid_chunk_k(j), (c, hkv, d), dtype) for j in range(2)]
+    V = [inputs.normal(15, inputs.tid_chunk_v(j), (c, hkv, d), dtype) for j in range(2)]
+    # oracle: each Q part over the union of KV parts (merged), gradients per KV part
+    ref = []
+    for i in range(2):
+        parts = [A.chunk_fwd(Q[i], K[j], V[j], offs[i], offs[j], True, 0.125) for j in range(2)]
+        ref.append(A.lse_merge(np.stack([p[0] for p in parts]), np.stack([p[1] for p in parts])))
+    gk = [np.zeros((c, hkv, d)) for _ in range(2)]
+    gv = [np.zeros((c, hkv, d)) for _ in range(2)]
+    gq = [np.zeros((c, hq, d)) for _ in range(2)]
+    acc = [torch.zeros(c, hq, d, device="cuda") for _ in range(2)]
+    dk = [torch.zeros(c, hkv, d, device="cuda") for _ in range(2)]
+    dv = [torch.zeros(c, hkv, d, device="cuda") for _ in range(2)]
+    for i in range(2):
+        o_in = torch.from_numpy(ref[i][0]).to(dtype)
+        l_in = torch.from_numpy(ref[i][1]).float()
+        for j in range(2):
+            a, b_, c_ = A.chunk_bwd(Q[i], K[j], V[j], o_in, l_in, dO[i], offs[i], offs[j], True, 0.125)
+            gq[i] += a
+            gk[j] += b_
+            gv[j] += c_
+            B.bs_attn_chunk_bwd(Q[i].cuda(), K[j].cuda(), V[j].cuda(), o_in.cuda(), l_in.cuda(),
+                                dO[i].cuda(), offs[i], offs[j], True, 0.125, acc[i], dk[j], dv[j],
+                                kv_accumulate=True)
+    bf = dtype == torch.bfloat16
+    tol = TOL[dtype]["grad"]
+    for j in range(2):
+        kf = B.bs_dq_finalize(dk[j], torch.empty(c, hkv, d, dtype=dtype, device="cuda"))
+        vf = B.bs_dq_finalize(dv[j], torch.empty(c, hkv, d, dtype=dtype, device="cuda"))
+        check_close(f"dK{j}", f64(kf), gk[j], tol, bf)
+        check_close(f"dV{j}", f64(vf), gv[j], tol, bf)
+        check_close(f"dQ{j}", f64(acc[j]), gq[j], tol)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_lse_merge_with_neg_inf_partials(gpu, dtype):
     n, T, hq, d = 5, 37, 3, 64
     rng = np.random.default_rng(12)

@@ -5,10 +5,10 @@
 // dq_bf16_kernel (query-major, walks the forward work list: 128-row query
 //   tiles over 64-key tiles).  Like the forward it keeps one query per lane,
 //   computing S^T = K Q^T and dP^T = V dO^T with Q and dO resident in
-//   registers (B operands) and K, V staged row-major in LDS (A operands);
+//   registers (B operands) and K, V tiles in LDS (A operands, row reads);
 //   P = exp2(S*scale*log2e - LSE*log2e), dS = P (dP - D) are per-lane fp32
 //   math; dQ^T += K^T dS^T takes dS^T straight from registers as the B operand
-//   and K^T from the same row-major K tile through transposing LDS reads
+//   and K^T from the same K tile through transposing LDS reads
 //   (ds_read_b64_tr_b16), which deliver the keys in the register order of dS^T.
 //   dQ is finished in registers and written once (bf16), or added to a float32
 //   accumulator for the context-parallel steps.
@@ -22,15 +22,22 @@
 //     P, dS                         (lane = one key, 16 query rows)
 //     dV^T += dO^T P,  dK^T += Q^T dS   (A = transposing reads of the same Q, dO
 //                                       tiles; B = P, dS straight from registers)
-//   K and V of the key tile stay in LDS for the whole item; query tiles are
-//   double-buffered: the next one is fetched into registers and written to the
-//   other buffer while the current one is consumed, one barrier per tile.  At
-//   the end the two waves of each key block add their partial sums through LDS.
-//   Query rows past the segment use LSE = +inf (P = 0), rows whose LSE is -inf
-//   (no visible key) also get P = 0.
+//   K and V of the key tile stay in LDS (row-major, padded) for the whole item;
+//   query tiles are XOR-swizzled (they are read both as rows and transposed)
+//   and double-buffered: the next one is fetched into registers and written to
+//   the other buffer while the current one is consumed, one barrier per tile.
+//   At the end the two waves of each key block add their partial sums through
+//   LDS.  Query rows past the segment use LSE = +inf (P = 0), rows whose LSE is
+//   -inf (no visible key) also get P = 0.
 //
-// All LDS staging is row-contiguous 16-byte traffic (no bank conflicts); rows
-// past a segment are fetched from its last valid row and never contribute.
+// The dQ kernel copies its tiles from HBM straight into LDS
+// (global_load_lds_dwordx4, no staging registers) into XOR-swizzled row-major
+// tiles (conflict-free for row reads and transposing reads alike), double-
+// buffered in distinct arrays: the copy of the next tile is issued before the
+// current one is consumed and waited for after it, one barrier per tile.  (The
+// dK/dV kernel keeps register staging: its accumulators leave no room for the
+// per-buffer LDS addresses that the direct copies need.)  Rows past a segment
+// are fetched from its last valid row and never contribute.
 #include "common.hpp"
 
 namespace bs {
@@ -66,13 +73,14 @@ template <int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void dq_bf16_kernel(const BwdParams p) {
   constexpr int BM = kFwdBM, BN = kFwdBN;
-  constexpr int NSTR = D + 8;   // K, V row-major tiles
+  constexpr int TILE = BN * D;   // swizzled [BN][D]
   constexpr int KK = D / 16, DB = D / 32;
-  constexpr int UNITS = BN * D / 8 / 256;  // 16-byte loads per thread per tensor
-  static_assert(BM == 128 && BN == 64 && UNITS >= 1, "tile shape");
+  static_assert(BM == 128 && BN == 64, "tile shape");
 
-  __shared__ __attribute__((aligned(16))) bf16 Ks[BN * NSTR];
-  __shared__ __attribute__((aligned(16))) bf16 Vs[BN * NSTR];
+  __shared__ __attribute__((aligned(16))) bf16 K0[TILE];
+  __shared__ __attribute__((aligned(16))) bf16 K1[TILE];
+  __shared__ __attribute__((aligned(16))) bf16 V0[TILE];
+  __shared__ __attribute__((aligned(16))) bf16 V1[TILE];
 
   const int item_idx = blockIdx.x / p.hq;
   if (item_idx >= p.hdr->n_items) return;
@@ -100,38 +108,18 @@ void dq_bf16_kernel(const BwdParams p) {
     lse2 = l == -INFINITY ? INFINITY : l * kLog2e;
     dval = p.dvec[(int64_t)h * p.total_q + it.a_start + qrow];
   }
-  wait_vmem_all();
 
   const bf16* kbase = p.k + (int64_t)it.b_start * kvstride + (int64_t)hk * D;
   const bf16* vbase = p.v + (int64_t)it.b_start * kvstride + (int64_t)hk * D;
   const int k_len = it.b_len;
   const int n_tiles = it.n1, n_full = it.n0;
 
-  bf16x8 kreg[UNITS], vreg[UNITS];
-  auto load_tile = [&](int t) {
+  auto copy_tile = [&](int t, bf16* Kd, bf16* Vd) {
     const int k0 = t * BN;
     const int last = k_len - 1 - k0;
-    const bf16* kt = kbase + (int64_t)k0 * kvstride;
-    const bf16* vt = vbase + (int64_t)k0 * kvstride;
-#pragma unroll
-    for (int i = 0; i < UNITS; ++i) {
-      const int idx = i * 256 + tid;
-      const int row = idx / (D / 8), ch = idx % (D / 8);
-      const int r = row < last ? row : last;
-      kreg[i] = *reinterpret_cast<const bf16x8*>(kt + r * kvstride + ch * 8);
-      vreg[i] = *reinterpret_cast<const bf16x8*>(vt + r * kvstride + ch * 8);
-    }
+    dma_tile<D, BN, 4>(Kd, kbase + (int64_t)k0 * kvstride, kvstride, last, w, lane);
+    dma_tile<D, BN, 4>(Vd, vbase + (int64_t)k0 * kvstride, kvstride, last, w, lane);
   };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < UNITS; ++i) {
-      const int idx = i * 256 + tid;
-      const int row = idx / (D / 8), ch = idx % (D / 8);
-      *reinterpret_cast<bf16x8*>(&Ks[row * NSTR + ch * 8]) = kreg[i];
-      *reinterpret_cast<bf16x8*>(&Vs[row * NSTR + ch * 8]) = vreg[i];
-    }
-  };
-  const bf16* ktr = tr_lane_ptr(Ks, NSTR, 0, 0, lane);  // K^T operand reads
 
   f32x16 dqacc[DB];
 #pragma unroll
@@ -142,12 +130,13 @@ void dq_bf16_kernel(const BwdParams p) {
   if (p.causal) lim_base = min(k_len, q_rel + it.diag + 1);
   lim_base -= hh * 4;
 
-  if (n_tiles > 0) load_tile(0);
-  for (int t = 0; t < n_tiles; ++t) {
-    __syncthreads();  // previous tile consumed
-    store_tile();
-    __syncthreads();
-    if (t + 1 < n_tiles) load_tile(t + 1);
+  if (n_tiles > 0) copy_tile(0, K0, V0);
+  wait_vmem_all();  // Q, dO fragments and tile 0
+  __syncthreads();
+
+  auto step = [&](int t, const bf16* Kb, const bf16* Vb, bf16* Kn, bf16* Vn) {
+    if (t + 1 < n_tiles) copy_tile(t + 1, Kn, Vn);
+    __builtin_amdgcn_sched_barrier(0);  // issue the copy before the reads below
 
     f32x16 sacc[2] = {f32x16{}, f32x16{}};
     f32x16 dpacc[2] = {f32x16{}, f32x16{}};
@@ -155,10 +144,10 @@ void dq_bf16_kernel(const BwdParams p) {
     for (int kk = 0; kk < KK; ++kk) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const int off = (kb * 32 + c) * NSTR + kk * 16 + hh * 8;
-        bf16x8 a = *reinterpret_cast<const bf16x8*>(&Ks[off]);
+        const int off = swz_off<D>(kb * 32 + c, kk * 2 + hh);
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Kb[off]);
         sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], sacc[kb], 0, 0, 0);
-        bf16x8 b = *reinterpret_cast<const bf16x8*>(&Vs[off]);
+        const bf16x8 b = *reinterpret_cast<const bf16x8*>(&Vb[off]);
         dpacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, dof[kk], dpacc[kb], 0, 0, 0);
       }
     }
@@ -183,10 +172,17 @@ void dq_bf16_kernel(const BwdParams p) {
     for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const bf16x8 a = lds_read_tr(ktr + ks * 16 * NSTR + db * 32, NSTR);
+        const bf16x8 a = lds_read_tr2(Kb + swz_tr_off<D>(ks * 16, db * 32, 0, lane),
+                                      Kb + swz_tr_off<D>(ks * 16, db * 32, 1, lane));
         dqacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[ks], dqacc[db], 0, 0, 0);
       }
     }
+    wait_vmem_all();  // this wave's copies of tile t+1
+    __syncthreads();
+  };
+  for (int t = 0; t < n_tiles; t += 2) {
+    step(t, K0, V0, K1, V1);
+    if (t + 1 < n_tiles) step(t + 1, K1, V1, K0, V0);
   }
 
   if (qvalid) {
@@ -218,8 +214,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void dkdv_bf16_kernel(const BwdParams p) {
   constexpr int BM = kBwdBM, BN = kBwdBN;
   constexpr int KK = D / 16, DB = D / 32;
-  constexpr int NSTR = D + 8;                 // row-major [row][d] tiles
-  constexpr int QTILE = BM * NSTR;
+  constexpr int NSTR = D + 8;                 // K, V row-major tiles (padded)
+  constexpr int QTILE = BM * D;               // Q, dO tiles: swizzled (read both ways)
   constexpr int KTILE = BN * NSTR;
   constexpr int NT = 512;
   constexpr int QUNITS = BM * D / 8 / NT;     // 16-byte loads per thread per Q/dO tile
@@ -313,8 +309,8 @@ void dkdv_bf16_kernel(const BwdParams p) {
     for (int u = 0; u < QUNITS; ++u) {
       const int idx = u * NT + tid;
       const int row = idx / (D / 8), ch = idx % (D / 8);
-      *reinterpret_cast<bf16x8*>(&Qs[buf * QTILE + row * NSTR + ch * 8]) = rq[u];
-      *reinterpret_cast<bf16x8*>(&dOs[buf * QTILE + row * NSTR + ch * 8]) = rd[u];
+      *reinterpret_cast<bf16x8*>(&Qs[buf * QTILE + swz_off<D>(row, ch)]) = rq[u];
+      *reinterpret_cast<bf16x8*>(&dOs[buf * QTILE + swz_off<D>(row, ch)]) = rd[u];
     }
     if (tid < BM) {
       lse_s[buf * BM + tid] = lse_r;
@@ -324,9 +320,7 @@ void dkdv_bf16_kernel(const BwdParams p) {
   // per-lane LDS offsets: rows of this wave's query half, its key block, and the
   // transposing reads of the query half
   const int qrow0 = qh * 32;
-  const int qoff = (qrow0 + c) * NSTR + hh * 8;
   const int koff = key_loc * NSTR + hh * 8;
-  const int tro = tr_lane_ptr(Qs, NSTR, qrow0, 0, lane) - Qs;
 
   if (n_iter > 0) {
     load_tile(0);
@@ -347,10 +341,10 @@ void dkdv_bf16_kernel(const BwdParams p) {
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[koff + kk * 16]);
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Qb[qoff + kk * 16]);
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Qb[swz_off<D>(qrow0 + c, kk * 2 + hh)]);
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kf, sacc, 0, 0, 0);
       const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vs[koff + kk * 16]);
-      const bf16x8 b = *reinterpret_cast<const bf16x8*>(&dOb[qoff + kk * 16]);
+      const bf16x8 b = *reinterpret_cast<const bf16x8*>(&dOb[swz_off<D>(qrow0 + c, kk * 2 + hh)]);
       dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, vf, dpacc, 0, 0, 0);
     }
 
@@ -372,16 +366,15 @@ void dkdv_bf16_kernel(const BwdParams p) {
       }
     }
 
-    const bf16* dOt = dOb + tro;
-    const bf16* Qt = Qb + tro;
 #pragma unroll
     for (int qs = 0; qs < 2; ++qs) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const int off = qs * 16 * NSTR + db * 32;
-        const bf16x8 a = lds_read_tr(dOt + off, NSTR);
+        const int o0 = swz_tr_off<D>(qrow0 + qs * 16, db * 32, 0, lane);
+        const int o1 = swz_tr_off<D>(qrow0 + qs * 16, db * 32, 1, lane);
+        const bf16x8 a = lds_read_tr2(dOb + o0, dOb + o1);
         dvacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[qs], dvacc[db], 0, 0, 0);
-        const bf16x8 b = lds_read_tr(Qt + off, NSTR);
+        const bf16x8 b = lds_read_tr2(Qb + o0, Qb + o1);
         dkacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, dsb[qs], dkacc[db], 0, 0, 0);
       }
     }

@@ -95,13 +95,77 @@ __device__ __forceinline__ const bf16* tr_lane_ptr(const bf16* tile, int stride,
   return tile + (k0 + (lane >> 5) * 4 + (i >> 2)) * stride + m0 + ((lane >> 4) & 1) * 16 + (i & 3) * 4;
 }
 
-// `p` is tr_lane_ptr(tile, stride, k0, m0, lane); the second read is 8 rows below.
-__device__ __forceinline__ bf16x8 lds_read_tr(const bf16* p, int stride) {
-  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
-  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * stride));
+// The operand from two lane addresses: rows k0 + hh*4 + (i/4) and the row 8 below.
+__device__ __forceinline__ bf16x8 lds_read_tr2(const bf16* p0, const bf16* p1) {
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p1));
   typedef short i16x8 __attribute__((ext_vector_type(8)));
   const i16x8 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
   return __builtin_bit_cast(bf16x8, v);
+}
+
+// `p` is tr_lane_ptr(tile, stride, k0, m0, lane) of a padded tile.
+__device__ __forceinline__ bf16x8 lds_read_tr(const bf16* p, int stride) {
+  return lds_read_tr2(p, p + 8 * stride);
+}
+
+// Swizzled row-major LDS tile with D bf16 per row (no padding) for tiles that are
+// read both ways: row reads (16 consecutive rows, one 16-byte chunk each) and
+// transposing reads (4 consecutive rows, 4 consecutive chunks each, per half
+// wave).  Chunk c of row r is stored at chunk c ^ g(r).  With 64 banks of 4
+// bytes, g makes both patterns conflict-free:
+//   D = 128 (16 chunks = one bank line per row): g(r) = ((r&3) << 2) | ((r>>2)&3)
+//     - any 16 consecutive rows: g is a bijection of r mod 16;
+//     - 4 aligned rows: (r&3) moves each row's 4-chunk group to a different quarter.
+//   D = 64 (8 chunks = half a bank line per row): g(r) = (((r>>1)&1) << 2) | ((r>>2)&3)
+//     - rows of equal parity share a half line, and g is a bijection over them;
+//     - of 4 aligned rows, the two of equal parity land in different 4-chunk groups.
+// g depends on r mod 16 only, so tiles may be addressed from any 16-row boundary.
+template <int D>
+__device__ __forceinline__ int swz_g(int r) {
+  static_assert(D == 64 || D == 128, "head_dim");
+  return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+}
+
+// Element offset of 16-byte chunk `c` of row `r`.
+template <int D>
+__device__ __forceinline__ int swz_off(int r, int c) {
+  return r * D + ((c ^ swz_g<D>(r)) << 3);
+}
+
+// One wave's share of copying rows 0..R-1 of a swizzled [R][D] bf16 tile from global
+// memory straight into LDS (global_load_lds_dwordx4: lane l of an instruction writes
+// 16 bytes at LDS base + 16*l, so an instruction fills 64/(D/8) whole rows and each
+// lane fetches the global chunk that the swizzle places at its LDS position).
+// Row r of the tile comes from src + min(r, last) * gstride elements: rows past the
+// end repeat the last valid one.  Completion is waited for with wait_vmem_all().
+template <int D, int R, int NWAVES>
+__device__ __forceinline__ void dma_tile(bf16* lds_tile, const bf16* src, int gstride, int last,
+                                         int wave, int lane) {
+  constexpr int CPR = D / 8, RPI = 64 / CPR, NI = R / RPI;
+  static_assert(NI % NWAVES == 0, "whole instructions per wave");
+  const int sub = lane / CPR, phys = lane % CPR;
+#pragma unroll
+  for (int k = 0; k < NI / NWAVES; ++k) {
+    const int u = k * NWAVES + wave;
+    const int row = u * RPI + sub;
+    const int r = row < last ? row : last;
+    const bf16* gp = src + (int64_t)r * gstride + ((phys ^ swz_g<D>(row)) << 3);
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)gp,
+                                     (__attribute__((address_space(3))) void*)(lds_tile + u * RPI * D),
+                                     16, 0, 0);
+  }
+}
+
+// Element offset, in a swizzled tile, of this lane's 8-byte piece of the transposing
+// read r (0 or 1) at contraction row k0 (a multiple of 16) and column m0 (a multiple
+// of 32): row k0 + 8r + 4hh + i/4, column m0 + 16*((lane/16)%2) + 4*(i%4).
+template <int D>
+__device__ __forceinline__ int swz_tr_off(int k0, int m0, int r, int lane) {
+  const int i = lane & 15;
+  const int row = k0 + 8 * r + 4 * (lane >> 5) + (i >> 2);
+  const int col = m0 + ((lane >> 4) & 1) * 16 + (i & 3) * 4;
+  return swz_off<D>(row, col >> 3) + (col & 7);
 }
 
 }  // namespace bs

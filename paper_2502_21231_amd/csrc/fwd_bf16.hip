@@ -12,28 +12,24 @@
 // over the lane's own registers plus one exchange with lane l^32, and the
 // output O^T = V^T P^T lands in the same "one query per lane" layout, so the
 // online-softmax rescale of O is a per-lane multiply.  P^T is fed back to the
-// MFMA straight from registers as the B operand; the contraction index order
-// that the register layout implies (within 16 keys: 0-3, 8-11 for lanes 0-31,
-// 4-7, 12-15 for lanes 32-63) is matched by storing V^T in LDS with the keys of
-// each 16-group permuted accordingly, so each A-operand read is one 16-byte
-// LDS load.
+// MFMA straight from registers as the B operand; V^T comes from transposing LDS
+// reads (ds_read_b64_tr_b16), which hand out the keys in exactly the order in
+// which the P^T registers hold them.
 //
-// Pipeline.  K and V tiles are staged row-major in LDS ([key][d]; K padded by 8
-// elements for the row reads of S^T = K Q^T, V by 32 for the transposing reads
-// (ds_read_b64_tr_b16) that hand out V^T in the permuted key order of P^T),
-// both double-buffered: while
-// tile t is consumed from one buffer, tile t+1 (already in registers) is
-// written to the other and tile t+2 is fetched from HBM, so there is one
-// barrier per key tile.  Key rows past the segment are fetched from the last
-// valid row (no zero-fill, so the global loads never have to be waited on
-// early) and are removed by the score mask, which every ragged tile has.
+// Pipeline.  K and V tiles are copied from HBM straight into LDS
+// (global_load_lds_dwordx4, no staging registers), into row-major tiles whose
+// 16-byte chunks are XOR-swizzled so that both the row reads of K and the
+// transposing reads of V are free of bank conflicts.  Both are double-buffered:
+// the copy of tile t+1 is issued before tile t is consumed and waited for after
+// it, one barrier per key tile.  Key rows past the segment are copied from the
+// last valid row and removed by the score mask, which every ragged tile has.
 //
 // Softmax.  Scores stay raw; the scale is folded into one FMA,
 // p = exp2(s * scale*log2(e) - m).  The running max m is only raised when a
 // tile's max exceeds it by more than 2^8 (in the exponent), so the O rescale
 // is skipped on almost every tile; p then stays below 2^8, which neither the
 // bf16 P nor the fp32 sums mind, and O = acc / l, LSE = (m + log2 l) ln 2 use
-// the same m.  All staging is row-contiguous 16-byte traffic (no bank conflicts).
+// the same m.
 #include "common.hpp"
 
 namespace bs {
@@ -66,16 +62,17 @@ template <int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void fwd_bf16_kernel(const FwdParams p) {
   constexpr int BM = kFwdBM, BN = kFwdBN;
-  constexpr int KSTR = D + 8;       // K tile row stride (elements)
-  constexpr int VSTR = D + 32;      // V tile row stride (transposing reads)
+  constexpr int TILE = BN * D;      // swizzled [BN][D] tile
   constexpr int KK = D / 16;        // MFMA k-steps over head_dim
   constexpr int DB = D / 32;        // 32-wide blocks of head_dim
-  constexpr int KUNITS = BN * D / 8 / 256;    // 16-byte K (and V) loads per thread
   static_assert(BM == 128 && BN == 64, "tile shape");
-  static_assert(KUNITS >= 1, "K staging");
 
-  __shared__ __attribute__((aligned(16))) bf16 Ks[2][BN * KSTR];
-  __shared__ __attribute__((aligned(16))) bf16 Vs[2][BN * VSTR];
+  // two buffers as distinct arrays, so that the compiler can tell the copy into one
+  // from the reads of the other and does not wait for the copy before reading
+  __shared__ __attribute__((aligned(16))) bf16 K0[TILE];
+  __shared__ __attribute__((aligned(16))) bf16 K1[TILE];
+  __shared__ __attribute__((aligned(16))) bf16 V0[TILE];
+  __shared__ __attribute__((aligned(16))) bf16 V1[TILE];
 
   const int item_idx = blockIdx.x / p.hq;
   if (item_idx >= p.hdr->n_items) return;
@@ -96,9 +93,6 @@ void fwd_bf16_kernel(const FwdParams p) {
     const bf16* qp = p.q + (int64_t)(it.a_start + (qvalid ? qrow : 0)) * qstride + (int64_t)h * D + hh * 8;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 16);
-    // Q must be resident before the key pipeline starts: otherwise the wait for it
-    // is merged, on the loop back-edge, with the wait for the tile being prefetched
-    wait_vmem_all();
   }
 
   const bf16* kbase = p.k + (int64_t)it.b_start * kvstride + (int64_t)hk * D;
@@ -106,31 +100,12 @@ void fwd_bf16_kernel(const FwdParams p) {
   const int k_len = it.b_len;
   const int n_tiles = it.n1, n_full = it.n0;
 
-  bf16x8 kreg[KUNITS], vreg[KUNITS];
-  auto load_tile = [&](int t) {
+  auto copy_tile = [&](int t, bf16* Kd, bf16* Vd) {
     const int k0 = t * BN;
     const int last = k_len - 1 - k0;  // last valid row inside the tile (>= 0)
-    const bf16* kt = kbase + (int64_t)k0 * kvstride;
-    const bf16* vt = vbase + (int64_t)k0 * kvstride;
-#pragma unroll
-    for (int i = 0; i < KUNITS; ++i) {
-      const int idx = i * 256 + tid;
-      const int row = idx / (D / 8), ch = idx % (D / 8);
-      const int r = row < last ? row : last;
-      kreg[i] = *reinterpret_cast<const bf16x8*>(kt + r * kvstride + ch * 8);
-      vreg[i] = *reinterpret_cast<const bf16x8*>(vt + r * kvstride + ch * 8);
-    }
+    dma_tile<D, BN, 4>(Kd, kbase + (int64_t)k0 * kvstride, kvstride, last, w, lane);
+    dma_tile<D, BN, 4>(Vd, vbase + (int64_t)k0 * kvstride, kvstride, last, w, lane);
   };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < KUNITS; ++i) {
-      const int idx = i * 256 + tid;
-      const int row = idx / (D / 8), ch = idx % (D / 8);
-      *reinterpret_cast<bf16x8*>(&Ks[buf][row * KSTR + ch * 8]) = kreg[i];
-      *reinterpret_cast<bf16x8*>(&Vs[buf][row * VSTR + ch * 8]) = vreg[i];
-    }
-  };
-  const int vtr = tr_lane_ptr(Vs[0], VSTR, 0, 0, lane) - Vs[0];  // this lane's V^T read offset
 
   f32x16 oacc[DB];
 #pragma unroll
@@ -144,24 +119,22 @@ void fwd_bf16_kernel(const FwdParams p) {
   if (p.causal) lim_base = min(k_len, q_rel + it.diag + 1);
   lim_base -= hh * 4;  // fold the lane-half offset of the key index
 
-  if (n_tiles > 0) {
-    load_tile(0);
-    store_tile(0);
-    if (n_tiles > 1) load_tile(1);
-  }
+  if (n_tiles > 0) copy_tile(0, K0, V0);
+  wait_vmem_all();  // Q fragment and tile 0
   __syncthreads();
 
-  for (int t = 0; t < n_tiles; ++t) {
-    const int buf = t & 1;
-    const bf16* Kb = Ks[buf];
-    const bf16* Vb = Vs[buf] + vtr;
+  // one key tile: consume (Kb, Vb) while tile t+1 is copied into (Kn, Vn), which
+  // were last read one tile earlier, before the barrier that ended it
+  auto step = [&](int t, const bf16* Kb, const bf16* Vb, bf16* Kn, bf16* Vn) {
+    if (t + 1 < n_tiles) copy_tile(t + 1, Kn, Vn);
+    __builtin_amdgcn_sched_barrier(0);  // issue the copy before the reads below
 
     f32x16 sacc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        bf16x8 a = *reinterpret_cast<const bf16x8*>(&Kb[(kb * 32 + c) * KSTR + kk * 16 + hh * 8]);
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Kb[swz_off<D>(kb * 32 + c, kk * 2 + hh)]);
         sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], sacc[kb], 0, 0, 0);
       }
     }
@@ -205,16 +178,18 @@ void fwd_bf16_kernel(const FwdParams p) {
     for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const bf16x8 a = lds_read_tr(Vb + ks * 16 * VSTR + db * 32, VSTR);
+        const bf16x8 a = lds_read_tr2(Vb + swz_tr_off<D>(ks * 16, db * 32, 0, lane),
+                                      Vb + swz_tr_off<D>(ks * 16, db * 32, 1, lane));
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[ks], oacc[db], 0, 0, 0);
       }
     }
 
-    if (t + 1 < n_tiles) {
-      store_tile(buf ^ 1);  // buffer buf^1 was last read in iteration t-1
-      if (t + 2 < n_tiles) load_tile(t + 2);
-    }
-    __syncthreads();
+    wait_vmem_all();  // this wave's copies of tile t+1
+    __syncthreads();  // everyone's copies landed; everyone is done with (Kb, Vb)
+  };
+  for (int t = 0; t < n_tiles; t += 2) {
+    step(t, K0, V0, K1, V1);
+    if (t + 1 < n_tiles) step(t + 1, K1, V1, K0, V0);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);

@@ -387,16 +387,16 @@ void dkdv_bf16_kernel(const BwdParams p) {
   }
 
   // sum the two query halves: waves 4..7 hand their partials to waves 0..3
-  f32x4* red = reinterpret_cast<f32x4*>(smem);  // [kbw][lane][2*DB*16 floats]
-  constexpr int PER_LANE = 2 * DB * 4;           // f32x4 per lane
+  // [kbw][2*DB*4 vectors][lane]: lane-minor, so a wave's accesses are contiguous
+  f32x4* red = reinterpret_cast<f32x4*>(smem) + kbw * (2 * DB * 4) * 64 + lane;
   if (qh == 1) {
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
-        red[(kbw * 64 + lane) * PER_LANE + db * 4 + a] =
+        red[(db * 4 + a) * 64] =
             f32x4{dvacc[db][a * 4], dvacc[db][a * 4 + 1], dvacc[db][a * 4 + 2], dvacc[db][a * 4 + 3]};
-        red[(kbw * 64 + lane) * PER_LANE + (DB + db) * 4 + a] =
+        red[((DB + db) * 4 + a) * 64] =
             f32x4{dkacc[db][a * 4], dkacc[db][a * 4 + 1], dkacc[db][a * 4 + 2], dkacc[db][a * 4 + 3]};
       }
   }
@@ -407,8 +407,8 @@ void dkdv_bf16_kernel(const BwdParams p) {
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
-        const f32x4 ov = red[(kbw * 64 + lane) * PER_LANE + db * 4 + a];
-        const f32x4 ok = red[(kbw * 64 + lane) * PER_LANE + (DB + db) * 4 + a];
+        const f32x4 ov = red[(db * 4 + a) * 64];
+        const f32x4 ok = red[((DB + db) * 4 + a) * 64];
         f32x4 gk, gv;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {

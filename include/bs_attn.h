@@ -35,7 +35,8 @@
  *   - Element type of Q/K/V/O/dO/dQ/dK/dV is dims->dtype: BS_BF16 (bf16 in,
  *     fp32 accumulation, round-to-nearest-even on every bf16 store) or BS_F32.
  *     LSE is always float32 (natural log).
- *   - head_dim must be 64 or 128; hq must be a multiple of hkv.
+ *   - head_dim must be 64 or 128; 1 <= hq <= 4096 and hq must be a multiple
+ *     of hkv.
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = default
  *     stream) and never synchronises the host, except the two test helpers
  *     bs_read_device_status() and bs_attn_plan_export().
@@ -61,7 +62,8 @@ extern "C" {
 
 typedef enum {
   BS_OK = 0,
-  BS_ERR_INVALID_ARG = 1,   /* null pointer, negative size, hq % hkv != 0, bad scale, n < 1 */
+  BS_ERR_INVALID_ARG = 1,   /* null pointer, negative size, hq out of range, hq % hkv != 0,
+                               bad scale, n < 1 */
   BS_ERR_UNSUPPORTED = 2,   /* head_dim not in {64, 128}, unknown dtype or op */
   BS_ERR_WORKSPACE = 3,     /* workspace pointer null or smaller than required */
   BS_ERR_HIP = 4,           /* a HIP runtime call failed (message names it) */

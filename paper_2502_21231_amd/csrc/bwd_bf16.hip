@@ -14,30 +14,35 @@
 //   accumulator for the context-parallel steps.
 //
 // dkdv_bf16_kernel (key-major, walks the backward work list: 128-key tiles
-//   over 64-row query tiles).  8 waves, 2 per SIMD: wave w owns the 32-key
-//   block w%4 of the tile and the query-row half w/4 of every query tile, and
-//   accumulates dK, dV of its keys in registers over all query heads of the KV
-//   group and all visible query tiles (MASKED diagonal tiles first):
-//     S  = Q K^T,  dP = dO V^T     (A = Q, dO rows; B = K, V rows; all from LDS)
-//     P, dS                         (lane = one key, 16 query rows)
-//     dV^T += dO^T P,  dK^T += Q^T dS   (A = transposing reads of the same Q, dO
-//                                       tiles; B = P, dS straight from registers)
-//   K and V of the key tile stay in LDS (row-major, padded) for the whole item;
-//   query tiles are XOR-swizzled (they are read both as rows and transposed)
-//   and double-buffered: the next one is fetched into registers and written to
-//   the other buffer while the current one is consumed, one barrier per tile.
-//   At the end the two waves of each key block add their partial sums through
-//   LDS.  Query rows past the segment use LSE = +inf (P = 0), rows whose LSE is
+//   over 64-row query tiles).  8 waves, 2 per SIMD, in pairs: both waves of
+//   pair b own the 32-key block b of the tile, and split the work by role.
+//     S wave  (holds K of its keys): S = Q K^T, P = exp2(S*c - LSE*log2e)
+//                                    (lane = one key, 64 query rows), hands P
+//                                    to its partner through LDS (fp32), and
+//                                    accumulates dV^T += dO^T P.
+//     dP wave (holds V of its keys): dP = dO V^T, dS = P (dP - D) with the P
+//                                    of its partner, dK^T += Q^T dS.
+//   Row operands (Q for S, dO for dP) are row reads of the query tiles, the
+//   transposed ones (dO^T, Q^T) transposing LDS reads of the same tiles; P and
+//   dS feed the MFMA straight from registers.  Each wave keeps only one of the
+//   two fragments and one of the two accumulators, which leaves registers for
+//   reading LDS operands several products ahead.  The S wave runs at raised
+//   priority through its products, so that its exponentials overlap the dP
+//   wave's products; the P hand-off is one LDS-only barrier per query tile,
+//   at which the copy of the next tile stays in flight.  dK, dV of every key are
+//   accumulated over all query heads of the KV group and all visible query
+//   tiles (MASKED diagonal tiles first) and written once.
+//   Query rows past the segment use LSE = +inf (P = 0), rows whose LSE is
 //   -inf (no visible key) also get P = 0.
 //
-// The dQ kernel copies its tiles from HBM straight into LDS
-// (global_load_lds_dwordx4, no staging registers) into XOR-swizzled row-major
-// tiles (conflict-free for row reads and transposing reads alike), double-
-// buffered in distinct arrays: the copy of the next tile is issued before the
-// current one is consumed and waited for after it, one barrier per tile.  (The
-// dK/dV kernel keeps register staging: its accumulators leave no room for the
-// per-buffer LDS addresses that the direct copies need.)  Rows past a segment
-// are fetched from its last valid row and never contribute.
+// Both kernels copy their tiles from HBM straight into LDS (buffer_load ... lds,
+// no staging registers) into XOR-swizzled row-major tiles (conflict-free for row
+// reads and transposing reads alike), double-buffered in distinct arrays: the
+// copy of the next tile is issued before the current one is consumed and waited
+// for after it, one full barrier per tile.  Rows past a segment are fetched from
+// its last valid row and never contribute.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace bs {
@@ -214,29 +219,21 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void dkdv_bf16_kernel(const BwdParams p) {
   constexpr int BM = kBwdBM, BN = kBwdBN;
   constexpr int KK = D / 16, DB = D / 32;
-  constexpr int NSTR = D + 8;                 // K, V row-major tiles (padded)
-  constexpr int QTILE = BM * D;               // Q, dO tiles: swizzled (read both ways)
-  constexpr int KTILE = BN * NSTR;
-  constexpr int NT = 512;
-  constexpr int QUNITS = BM * D / 8 / NT;     // 16-byte loads per thread per Q/dO tile
-  constexpr int KUNITS = BN * D / 8 / NT;     // 16-byte loads per thread per K/V tile
-  static_assert(BM == 64 && BN == 128 && QUNITS >= 1, "tile shape");
-  // LDS: K, V of the key tile (resident), Q and dO query tiles (double-buffered),
-  // LSE / D rows.  After the loop the same space holds the partial dK, dV of
-  // the waves that own the second half of each query tile.
-  constexpr int KV_BYTES = 2 * KTILE * 2;
-  constexpr int Q_BYTES = 2 * 2 * QTILE * 2;
-  constexpr int ROW_BYTES = 2 * 2 * BM * 4;
-  constexpr int RED_BYTES = 4 * 64 * 2 * DB * 16 * 4;
-  constexpr int SMEM = (KV_BYTES + Q_BYTES + ROW_BYTES) > RED_BYTES ? (KV_BYTES + Q_BYTES + ROW_BYTES)
-                                                                    : RED_BYTES;
-  __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  bf16* Ks = reinterpret_cast<bf16*>(smem);
-  bf16* Vs = Ks + KTILE;
-  bf16* Qs = Vs + KTILE;            // [2][QTILE]
-  bf16* dOs = Qs + 2 * QTILE;       // [2][QTILE]
-  float* lse_s = reinterpret_cast<float*>(dOs + 2 * QTILE);  // [2][BM]
-  float* dvec_s = lse_s + 2 * BM;                            // [2][BM]
+  constexpr int MB = BM / 32;                 // 32-row blocks of a query tile
+  constexpr int QS = BM / 16;                 // 16-row contraction steps of a query tile
+  constexpr int QTILE = BM * D;               // swizzled [BM][D] query tile
+  constexpr int NW = 8;
+  static_assert(BM == 64 && BN == 128, "tile shape");
+  // Q and dO tiles, double-buffered; each buffer is its own array (Q tile, then
+  // dO tile), so that the compiler can tell the copy into one from the reads of
+  // the other
+  __shared__ __attribute__((aligned(16))) bf16 QD0[2 * QTILE];
+  __shared__ __attribute__((aligned(16))) bf16 QD1[2 * QTILE];
+  // LSE (log2 units) then D rows of the query tile, double-buffered
+  __shared__ __attribute__((aligned(16))) float R0[2 * BM];
+  __shared__ __attribute__((aligned(16))) float R1[2 * BM];
+  // P handed from the S wave to the dP wave of each key block: [block][vector][lane]
+  __shared__ __attribute__((aligned(16))) f32x4 Ps[4 * MB * 4 * 64];
 
   const int item_idx = blockIdx.x / p.hkv;
   if (item_idx >= p.hdr->n_items) return;
@@ -245,187 +242,200 @@ void dkdv_bf16_kernel(const BwdParams p) {
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, c = lane & 31, hh = lane >> 5;
-  const int kbw = w & 3;           // this wave's 32-key block of the tile
-  const int qh = w >> 2;           // this wave's 32-row half of every query tile
+  const int kb = w & 3;     // this wave's 32-key block of the tile
+  const int role = w >> 2;  // 0: S, P, dV (holds K)    1: dP, dS, dK (holds V)
   const int64_t qstride = (int64_t)p.hq * D;
   const int kvstride = p.hkv * D;
   const int k_rows = it.a_rows;
-  const int key_loc = kbw * 32 + c;
+  const int key_loc = kb * 32 + c;
+  const bool kvalid = key_loc < k_rows;
   const int key_rel = it.tile * BN + key_loc;   // key index inside its segment
 
-  // K, V of the key tile, row-major (rows past the segment repeat its last key)
+  // this lane's K row (role 0) or V row (role 1): B operand of S = Q K^T, dP = dO V^T
+  bf16x8 frag[KK];
   {
-    const bf16* kb = p.k + (int64_t)it.a_start * kvstride + (int64_t)hk * D;
-    const bf16* vb = p.v + (int64_t)it.a_start * kvstride + (int64_t)hk * D;
+    const bf16* src = role == 0 ? p.k : p.v;
+    const bf16* rp = src + (int64_t)(it.a_start + (kvalid ? key_loc : 0)) * kvstride +
+                     (int64_t)hk * D + hh * 8;
 #pragma unroll
-    for (int u = 0; u < KUNITS; ++u) {
-      const int idx = u * NT + tid;
-      const int row = idx / (D / 8), ch = idx % (D / 8);
-      const int r = row < k_rows - 1 ? row : k_rows - 1;
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kb + r * kvstride + ch * 8);
-      const bf16x8 b = *reinterpret_cast<const bf16x8*>(vb + r * kvstride + ch * 8);
-      *reinterpret_cast<bf16x8*>(&Ks[row * NSTR + ch * 8]) = a;
-      *reinterpret_cast<bf16x8*>(&Vs[row * NSTR + ch * 8]) = b;
-    }
+    for (int kk = 0; kk < KK; ++kk) frag[kk] = *reinterpret_cast<const bf16x8*>(rp + kk * 16);
   }
-
-  f32x16 dvacc[DB], dkacc[DB];
+  // dV^T (role 0) or unscaled dK^T (role 1) of this lane's key: column c, rows d
+  f32x16 acc[DB];
 #pragma unroll
-  for (int db = 0; db < DB; ++db) { dvacc[db] = f32x16{}; dkacc[db] = f32x16{}; }
+  for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
 
   const int q_len = it.b_len;
   const int qt_first = it.n0, n_masked = it.n1, n_vis = it.n2;
   const int diag = it.diag;
   const int n_iter = n_vis * p.group;
 
-  bf16x8 rq[QUNITS], rd[QUNITS];
-  float lse_r = INFINITY, dv_r = 0.f;
-  auto load_tile = [&](int i) {
+  // All eight waves copy query tile i (head, rows) into QDd; the first dP wave
+  // fetches its LSE rows, the second its D rows.
+  const int ct = tid - 4 * 64;  // thread index among the role-1 waves
+  float row_r = 0.f;   // raw LSE / D value of one row (converted when stored)
+  bool row_ok = false;  // the row lies inside the segment
+  auto copy_tile = [&](int i, bf16* QDd) {
     const int hg = i / n_vis, j = i - hg * n_vis;
     const int h = hk * p.group + hg;
     const int q_rel0 = (qt_first + j) * BM;
     const int64_t q_glob0 = (int64_t)it.b_start + q_rel0;
     const int last = q_len - 1 - q_rel0;
-    const bf16* qp = p.q + q_glob0 * qstride + (int64_t)h * D;
-    const bf16* dp = p.dout + q_glob0 * qstride + (int64_t)h * D;
-#pragma unroll
-    for (int u = 0; u < QUNITS; ++u) {
-      const int idx = u * NT + tid;
-      const int row = idx / (D / 8), ch = idx % (D / 8);
-      const int64_t ro = (int64_t)(row < last ? row : last) * qstride + ch * 8;
-      rq[u] = *reinterpret_cast<const bf16x8*>(qp + ro);
-      rd[u] = *reinterpret_cast<const bf16x8*>(dp + ro);
-    }
-    if (tid < BM) {
-      const bool ok = tid <= last;
-      const int64_t li = (int64_t)h * p.total_q + q_glob0 + (ok ? tid : 0);
-      const float l = p.lse[li];
-      lse_r = (!ok || l == -INFINITY) ? INFINITY : l * kLog2e;
-      dv_r = ok ? p.dvec[li] : 0.f;
+    const int64_t qo = q_glob0 * qstride + (int64_t)h * D;
+    dma_tile<D, BM, NW>(QDd, p.q + qo, (int)qstride, last, w, lane);
+    dma_tile<D, BM, NW>(QDd + QTILE, p.dout + qo, (int)qstride, last, w, lane);
+    if (ct >= 0 && ct < 2 * BM) {
+      const int r = ct & (BM - 1);
+      row_ok = r <= last;
+      const int64_t li = (int64_t)h * p.total_q + q_glob0 + (row_ok ? r : 0);
+      row_r = (ct < BM ? p.lse : p.dvec)[li];
     }
   };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < QUNITS; ++u) {
-      const int idx = u * NT + tid;
-      const int row = idx / (D / 8), ch = idx % (D / 8);
-      *reinterpret_cast<bf16x8*>(&Qs[buf * QTILE + swz_off<D>(row, ch)]) = rq[u];
-      *reinterpret_cast<bf16x8*>(&dOs[buf * QTILE + swz_off<D>(row, ch)]) = rd[u];
-    }
-    if (tid < BM) {
-      lse_s[buf * BM + tid] = lse_r;
-      dvec_s[buf * BM + tid] = dv_r;
-    }
+  // LSE rows in log2 units, +inf (P = 0) past the segment and where no key is visible
+  auto store_rows = [&](float* Rd) {
+    if (ct < BM)
+      Rd[ct] = (!row_ok || row_r == -INFINITY) ? INFINITY : row_r * kLog2e;
+    else if (ct < 2 * BM)
+      Rd[ct] = row_ok ? row_r : 0.f;
   };
-  // per-lane LDS offsets: rows of this wave's query half, its key block, and the
-  // transposing reads of the query half
-  const int qrow0 = qh * 32;
-  const int koff = key_loc * NSTR + hh * 8;
 
-  if (n_iter > 0) {
-    load_tile(0);
-    store_tile(0);
-    if (n_iter > 1) load_tile(1);
-  }
+  if (n_iter > 0) copy_tile(0, QD0);
+  wait_vmem_all();  // K / V row, tile 0 and its rows
+  if (role == 1 && n_iter > 0) store_rows(R0);
   __syncthreads();
 
-  for (int i = 0; i < n_iter; ++i) {
-    const int buf = i & 1;
+  // phase 1 reads rows of Q (role 0) or dO (role 1); phase 2 reads dO (role 0)
+  // or Q (role 1) transposed
+  const int base1 = role * QTILE, base2 = (1 - role) * QTILE;
+  f32x4* pslot = Ps + kb * (MB * 4) * 64 + lane;
+
+  // one query tile: consume (QDb, Rb) while tile i+1 is copied into (QDn, Rn),
+  // which were last read one tile earlier, before the barrier that ended it
+  auto step = [&](int i, const bf16* QDb, const float* Rb, bf16* QDn, float* Rn) {
+    if (i + 1 < n_iter) copy_tile(i + 1, QDn);
+    __builtin_amdgcn_sched_barrier(0);  // issue the copy before the reads below
     const int hg = i / n_vis, j = i - hg * n_vis;
     const int q_rel0 = (qt_first + j) * BM;
     const bool masked = j < n_masked;
-    const bf16* Qb = Qs + buf * QTILE;
-    const bf16* dOb = dOs + buf * QTILE;
+    const bf16* A1 = QDb + base1;
+    const bf16* A2 = QDb + base2;
 
-    f32x16 sacc = f32x16{}, dpacc = f32x16{};
+    // S = Q K^T (role 0) or dP = dO V^T (role 1): lane = key, rows q = mb*32 + (r/4)*8 + hh*4 + r%4
+    // (the S wave goes first on the matrix unit, so that its exponentials overlap
+    // the dP wave's products)
+    if (role == 0) __builtin_amdgcn_s_setprio(1);
+    f32x16 s[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) s[mb] = f32x16{};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[koff + kk * 16]);
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Qb[swz_off<D>(qrow0 + c, kk * 2 + hh)]);
-      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kf, sacc, 0, 0, 0);
-      const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vs[koff + kk * 16]);
-      const bf16x8 b = *reinterpret_cast<const bf16x8*>(&dOb[swz_off<D>(qrow0 + c, kk * 2 + hh)]);
-      dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, vf, dpacc, 0, 0, 0);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&A1[swz_off<D>(mb * 32 + c, kk * 2 + hh)]);
+        s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, frag[kk], s[mb], 0, 0, 0);
+      }
+    }
+    // keep the row reads two contraction steps ahead of the products
+    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * MB, 0);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, MB, 0);
+      if (kk + 2 < KK) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, MB, 0);
     }
 
-    bf16x8 pb[2], dsb[2];
-    // lane = key key_loc, rows q = qrow0 + a4*8 + hh*4 + e
-    const int vis_lim = key_rel - diag - q_rel0 - hh * 4;  // visible iff row >= vis_lim
+    // B operand of phase 2: P (role 0) or dS (role 1), 16-row step qs = mb*2 + r/8
+    bf16x8 ob[QS];
+    if (role == 0) {
+      __builtin_amdgcn_s_setprio(0);
+      // P = exp2(S * scale * log2(e) - LSE * log2(e)); on MASKED tiles of a causal
+      // pass, rows above the diagonal (row < vis_lim) are zeroed
+      auto softmax = [&](auto use_mask) {
+        const int vis_lim = key_rel - diag - q_rel0 - hh * 4;
 #pragma unroll
-    for (int a4 = 0; a4 < 4; ++a4) {
-      const int ql = qrow0 + a4 * 8 + hh * 4;
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse_s[buf * BM + ql]);
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dvec_s[buf * BM + ql]);
+        for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = a4 * 4 + e;
-        float pr = fast_exp2(fmaf(sacc[r], p.scale_log2, -l4[e]));
-        if (masked && p.causal) pr = (qrow0 + a4 * 8 + e) >= vis_lim ? pr : 0.f;
-        pb[r >> 3][r & 7] = f2bf(pr);
-        dsb[r >> 3][r & 7] = f2bf(pr * (dpacc[r] - d4[e]));
+          for (int a4 = 0; a4 < 4; ++a4) {
+            const f32x4 l4 = *reinterpret_cast<const f32x4*>(&Rb[mb * 32 + a4 * 8 + hh * 4]);
+            f32x4 pv;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int r = a4 * 4 + e;
+              float pr = fast_exp2(fmaf(s[mb][r], p.scale_log2, -l4[e]));
+              if (decltype(use_mask)::value) pr = (mb * 32 + a4 * 8 + e) >= vis_lim ? pr : 0.f;
+              pv[e] = pr;
+              ob[mb * 2 + (r >> 3)][r & 7] = f2bf(pr);
+            }
+            pslot[(mb * 4 + a4) * 64] = pv;
+          }
+        }
+      };
+      if (masked && p.causal)
+        softmax(std::true_type{});
+      else
+        softmax(std::false_type{});
+    }
+    barrier_lds();  // P of every key block is in LDS (the copies of tile i+1 stay in flight)
+    if (role == 1) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) {
+          const f32x4 d4 = *reinterpret_cast<const f32x4*>(&Rb[BM + mb * 32 + a4 * 8 + hh * 4]);
+          const f32x4 pv = pslot[(mb * 4 + a4) * 64];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = a4 * 4 + e;
+            ob[mb * 2 + (r >> 3)][r & 7] = f2bf(pv[e] * (s[mb][r] - d4[e]));
+          }
+        }
       }
     }
 
+    // dV^T += dO^T P (role 0) or dK^T += Q^T dS (role 1)
 #pragma unroll
-    for (int qs = 0; qs < 2; ++qs) {
+    for (int qs = 0; qs < QS; ++qs) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const int o0 = swz_tr_off<D>(qrow0 + qs * 16, db * 32, 0, lane);
-        const int o1 = swz_tr_off<D>(qrow0 + qs * 16, db * 32, 1, lane);
-        const bf16x8 a = lds_read_tr2(dOb + o0, dOb + o1);
-        dvacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[qs], dvacc[db], 0, 0, 0);
-        const bf16x8 b = lds_read_tr2(Qb + o0, Qb + o1);
-        dkacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, dsb[qs], dkacc[db], 0, 0, 0);
+        const bf16x8 a = lds_read_tr2(A2 + swz_tr_off<D>(qs * 16, db * 32, 0, lane),
+                                      A2 + swz_tr_off<D>(qs * 16, db * 32, 1, lane));
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ob[qs], acc[db], 0, 0, 0);
       }
     }
-
-    if (i + 1 < n_iter) {
-      store_tile(buf ^ 1);  // buffer buf^1 was last read in iteration i-1
-      if (i + 2 < n_iter) load_tile(i + 2);
+    // keep the transposing reads three products ahead
+    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 6, 1);
+#pragma unroll
+    for (int m = 0; m < QS * DB; ++m) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 1);
+      if (m + 3 < QS * DB) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 1);
     }
+    wait_vmem_all();  // this wave's copies of tile i+1 and its rows
+    if (role == 1 && i + 1 < n_iter) store_rows(Rn);
     __syncthreads();
+  };
+  for (int i = 0; i < n_iter; i += 2) {
+    step(i, QD0, R0, QD1, R1);
+    if (i + 1 < n_iter) step(i + 1, QD1, R1, QD0, R0);
   }
 
-  // sum the two query halves: waves 4..7 hand their partials to waves 0..3
-  // [kbw][2*DB*4 vectors][lane]: lane-minor, so a wave's accesses are contiguous
-  f32x4* red = reinterpret_cast<f32x4*>(smem) + kbw * (2 * DB * 4) * 64 + lane;
-  if (qh == 1) {
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        red[(db * 4 + a) * 64] =
-            f32x4{dvacc[db][a * 4], dvacc[db][a * 4 + 1], dvacc[db][a * 4 + 2], dvacc[db][a * 4 + 3]};
-        red[((DB + db) * 4 + a) * 64] =
-            f32x4{dkacc[db][a * 4], dkacc[db][a * 4 + 1], dkacc[db][a * 4 + 2], dkacc[db][a * 4 + 3]};
-      }
-  }
-  __syncthreads();
-  if (qh == 0 && key_loc < k_rows) {
+  if (kvalid) {
     const int64_t off = (int64_t)(it.a_start + key_loc) * kvstride + (int64_t)hk * D + hh * 4;
+    const float mul = role == 0 ? 1.f : p.scale;
+    float* gacc = role == 0 ? p.dv_acc : p.dk_acc;
+    bf16* gout = role == 0 ? p.dv : p.dk;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
-        const f32x4 ov = red[(db * 4 + a) * 64];
-        const f32x4 ok = red[((DB + db) * 4 + a) * 64];
-        f32x4 gk, gv;
+        f32x4 g;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          gk[e] = (dkacc[db][a * 4 + e] + ok[e]) * p.scale;
-          gv[e] = dvacc[db][a * 4 + e] + ov[e];
-        }
+        for (int e = 0; e < 4; ++e) g[e] = acc[db][a * 4 + e] * mul;
         const int col = db * 32 + a * 8;
-        if (p.dk_acc != nullptr) {  // add into float32 accumulators
-          f32x4* dk4 = reinterpret_cast<f32x4*>(p.dk_acc + off + col);
-          f32x4* dv4 = reinterpret_cast<f32x4*>(p.dv_acc + off + col);
-          *dk4 = *dk4 + gk;
-          *dv4 = *dv4 + gv;
+        if (gacc != nullptr) {  // add into float32 accumulators
+          f32x4* dst = reinterpret_cast<f32x4*>(gacc + off + col);
+          *dst = *dst + g;
         } else {
-          const bf16x4 xk = {f2bf(gk[0]), f2bf(gk[1]), f2bf(gk[2]), f2bf(gk[3])};
-          const bf16x4 xv = {f2bf(gv[0]), f2bf(gv[1]), f2bf(gv[2]), f2bf(gv[3])};
-          *reinterpret_cast<bf16x4*>(p.dk + off + col) = xk;
-          *reinterpret_cast<bf16x4*>(p.dv + off + col) = xv;
+          const bf16x4 x = {f2bf(g[0]), f2bf(g[1]), f2bf(g[2]), f2bf(g[3])};
+          *reinterpret_cast<bf16x4*>(gout + off + col) = x;
         }
       }
     }

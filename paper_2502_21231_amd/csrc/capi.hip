@@ -34,6 +34,8 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 constexpr int64_t kMaxTokens = int64_t(1) << 30;
+// query heads: keeps the byte offsets inside one tile of rows below 2^31
+constexpr int32_t kMaxHeads = 4096;
 
 // Profiling: pairs of HIP events recorded around each kernel launch while enabled.
 struct Profiler {
@@ -117,7 +119,8 @@ int check_dims(const bs_dims* d, bool need_kv) {
     return fail(BS_ERR_UNSUPPORTED, "dtype %d is not BS_F32 or BS_BF16", d->dtype);
   if (d->head_dim != 64 && d->head_dim != 128)
     return fail(BS_ERR_UNSUPPORTED, "head_dim %d is not 64 or 128", d->head_dim);
-  if (d->hq < 1) return fail(BS_ERR_INVALID_ARG, "hq = %d must be >= 1", d->hq);
+  if (d->hq < 1 || d->hq > kMaxHeads)
+    return fail(BS_ERR_INVALID_ARG, "hq = %d out of [1, %d]", d->hq, kMaxHeads);
   if (d->total_q < 0 || d->total_q >= kMaxTokens)
     return fail(BS_ERR_INVALID_ARG, "total_q = %lld out of [0, 2^30)", (long long)d->total_q);
   if (need_kv) {

@@ -71,6 +71,17 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // wave's outstanding vector-memory loads have returned.
 __device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// Workgroup barrier that orders LDS traffic only: waits for this wave's LDS
+// operations (lgkmcnt) but not for its outstanding global loads, so that copies
+// into another buffer stay in flight across it.  The memory clobber keeps the
+// compiler from moving memory operations across it.
+__device__ __forceinline__ void barrier_lds() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008, kSchedDsRead = 0x100;
+
 // Operand of a 32x32x16 bf16 MFMA that is the TRANSPOSE of a row-major LDS tile.
 //
 // X is a row-major bf16 tile in LDS (`stride` elements per row) whose rows run
@@ -134,26 +145,33 @@ __device__ __forceinline__ int swz_off(int r, int c) {
 }
 
 // One wave's share of copying rows 0..R-1 of a swizzled [R][D] bf16 tile from global
-// memory straight into LDS (global_load_lds_dwordx4: lane l of an instruction writes
-// 16 bytes at LDS base + 16*l, so an instruction fills 64/(D/8) whole rows and each
-// lane fetches the global chunk that the swizzle places at its LDS position).
+// memory straight into LDS (buffer_load_dwordx4 ... lds: lane l of an instruction
+// writes 16 bytes at LDS base + 16*l, so an instruction fills 64/(D/8) whole rows and
+// each lane fetches the global chunk that the swizzle places at its LDS position).
 // Row r of the tile comes from src + min(r, last) * gstride elements: rows past the
 // end repeat the last valid one.  Completion is waited for with wait_vmem_all().
+//
+// The buffer form (MUBUF) rather than global_load_lds (FLAT): the compiler treats a
+// pending FLAT copy into LDS as a possible LDS access of unknown order and then
+// waits for all LDS reads (lgkmcnt(0)) before every use, which defeats reading LDS
+// operands ahead.  The buffer is the tile's rows from `src`; byte offsets
+// (R rows x gstride x 2) stay below 2^31 for the head counts the C API accepts.
 template <int D, int R, int NWAVES>
 __device__ __forceinline__ void dma_tile(bf16* lds_tile, const bf16* src, int gstride, int last,
                                          int wave, int lane) {
   constexpr int CPR = D / 8, RPI = 64 / CPR, NI = R / RPI;
   static_assert(NI % NWAVES == 0, "whole instructions per wave");
   const int sub = lane / CPR, phys = lane % CPR;
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void*)src, 0, 0x7fffffff, 0x00020000);
 #pragma unroll
   for (int k = 0; k < NI / NWAVES; ++k) {
     const int u = k * NWAVES + wave;
     const int row = u * RPI + sub;
     const int r = row < last ? row : last;
-    const bf16* gp = src + (int64_t)r * gstride + ((phys ^ swz_g<D>(row)) << 3);
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)gp,
-                                     (__attribute__((address_space(3))) void*)(lds_tile + u * RPI * D),
-                                     16, 0, 0);
+    const int voff = (r * gstride + ((phys ^ swz_g<D>(row)) << 3)) * 2;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(lds_tile + u * RPI * D),
+                                             16, voff, 0, 0, 0);
   }
 }
 

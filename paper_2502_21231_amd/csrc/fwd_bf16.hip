@@ -17,7 +17,7 @@
 // which the P^T registers hold them.
 //
 // Pipeline.  K and V tiles are copied from HBM straight into LDS
-// (global_load_lds_dwordx4, no staging registers), into row-major tiles whose
+// (buffer_load_dwordx4 ... lds, no staging registers), into row-major tiles whose
 // 16-byte chunks are XOR-swizzled so that both the row reads of K and the
 // transposing reads of V are free of bank conflicts.  Both are double-buffered:
 // the copy of tile t+1 is issued before tile t is consumed and waited for after

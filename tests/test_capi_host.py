@@ -53,6 +53,7 @@ def test_rejects_bad_arguments_without_device(lib):
     assert fwd(lib, dims(dtype=7)) == B.BS_ERR_UNSUPPORTED
     assert fwd(lib, dims(hq=6, hkv=4)) == B.BS_ERR_INVALID_ARG
     assert fwd(lib, dims(hkv=0)) == B.BS_ERR_INVALID_ARG
+    assert fwd(lib, dims(hq=8192, hkv=8)) == B.BS_ERR_INVALID_ARG  # above the 4096-head limit
     assert fwd(lib, dims(total_q=-1)) == B.BS_ERR_INVALID_ARG
     assert fwd(lib, dims(), q=None) == B.BS_ERR_INVALID_ARG
     assert "q is NULL" in B.bs_last_error()

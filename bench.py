@@ -26,6 +26,38 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 BF16_PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12   # 2516.6: MI355X dense bf16 MFMA (AMD's 2.5 PF)
+REPO = os.path.dirname(os.path.abspath(__file__))
+# sources whose text fixes each timed kernel (a counter record applies only to them)
+KERNEL_SOURCES = {"fwd": ["fwd_bf16.hip", "common.hpp"], "bwd_dq": ["bwd_bf16.hip", "common.hpp"],
+                  "bwd_dkdv": ["bwd_bf16.hip", "common.hpp"]}
+
+
+def kernel_source_hash(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(REPO, "paper_2502_21231_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` on `workload` from the counter record in a
+    profiles/*.md summary (a fenced json block with a "traffic_record" key), or None
+    when there is no record or the kernel's sources changed since it was taken."""
+    import glob
+    want = kernel_source_hash(kernel)
+    for path in sorted(glob.glob(os.path.join(REPO, "profiles", "*.md"))):
+        text = open(path).read()
+        for block in text.split("```json")[1:]:
+            try:
+                rec = json.loads(block.split("```")[0])
+            except ValueError:
+                continue
+            for r in rec.get("traffic_record", []):
+                if r.get("workload") == workload and r.get("kernel") == kernel and r.get("source_sha256") == want:
+                    return r["read_bytes"] + r["write_bytes"]
+    return None
 HBM_PEAK_GBS = 8000.0
 
 WORKLOADS = {
@@ -151,7 +183,9 @@ def time_steps(step, args, dev, flops_fwd, flops_bwd):
         "kernels": kern,
         "roofline": {"kernel": f"bs_attn {dom} (bf16 MFMA)", "bound": "mfma", "achieved": achieved,
                      "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": achieved / BF16_PEAK_TFLOPS,
-                     "traffic": None},
+                     # HBM bytes (read + write) per launch, from the FETCH_SIZE / WRITE_SIZE
+                     # record in profiles/ (null when the kernel changed since)
+                     "traffic": recorded_traffic(args.workload, dom)},
     }
 
 

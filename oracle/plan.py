@@ -21,13 +21,17 @@ The tests pin this corner rule against an enumeration of every (i, j) pair.
 
 Forward items are query tiles: (seg, qtile, q_start, q_rows, k_start, k_len,
 n_full, n_tiles, diag), the visible key tiles being 0..n_tiles-1 of which the
-first n_full are FULL.  They are ordered by n_tiles descending, ties by
-(seg, qtile) ascending.
+first n_full are FULL.
 
 Backward items are key tiles: (seg, ktile, k_start, k_rows, q_start, q_len,
 qt_first, n_masked, n_vis, diag), the visible query tiles being qt_first ..
-qt_first+n_vis-1 of which the first n_masked are MASKED.  They are ordered by
-n_vis descending, ties by (seg, ktile) ascending.
+qt_first+n_vis-1 of which the first n_masked are MASKED.
+
+Order of the list (largest work first, the tiles of one segment side by side):
+segments by len_q + len_k descending, ties by segment index; inside a segment,
+forward query tiles by descending index, backward key tiles by ascending index.
+Inside a segment that is descending cost (n_tiles, n_vis), which the tests check
+against the counts themselves.
 """
 from __future__ import annotations
 
@@ -115,14 +119,15 @@ def bwd_items_for_segment(b, q0, lq, k0, lk, diag, causal, BM, BN):
 
 def varlen_plan(cu_q, cu_k, causal, BM, BN, kind="fwd"):
     """Ordered work list of a packed buffer (kind 'fwd' = query tiles, 'bwd' = key tiles)."""
-    items = []
+    items, size = [], {}
     for b, q0, lq, k0, lk in _segments(cu_q, cu_k):
         diag = lk - lq
+        size[b] = lq + lk
         if kind == "fwd":
             items += fwd_items_for_segment(b, q0, lq, k0, lk, diag, causal, BM, BN)
         else:
             items += bwd_items_for_segment(b, q0, lq, k0, lk, diag, causal, BM, BN)
-    return _order(items, kind)
+    return _order(items, kind, size)
 
 
 def chunk_plan(len_q, len_k, q_off, k_off, causal, BM, BN, kind="fwd"):
@@ -132,13 +137,14 @@ def chunk_plan(len_q, len_k, q_off, k_off, causal, BM, BN, kind="fwd"):
         items = fwd_items_for_segment(0, 0, len_q, 0, len_k, diag, causal, BM, BN)
     else:
         items = bwd_items_for_segment(0, 0, len_q, 0, len_k, diag, causal, BM, BN)
-    return _order(items, kind)
+    return _order(items, kind, {0: len_q + len_k})
 
 
-def _order(items, kind):
-    if kind == "fwd":
-        return sorted(items, key=lambda it: (-it[7], it[0], it[1]))
-    return sorted(items, key=lambda it: (-it[8], it[0], it[1]))
+def _order(items, kind, size):
+    """Segments by size descending (ties: index), then forward tiles by descending
+    index, backward tiles by ascending index."""
+    sign = -1 if kind == "fwd" else 1
+    return sorted(items, key=lambda it: (-size[it[0]], it[0], sign * it[1]))
 
 
 def tile_counts(items, kind="fwd"):

@@ -158,8 +158,8 @@ WsLayout layout_of(int op, const bs_dims& d, int64_t nseg) {
   size_t off = align256(sizeof(WsHeader));
   L.seg_off = off;
   off += align256(sizeof(int32_t) * (size_t)(nseg + 2));
-  L.unsorted = off;
-  off += align256(sizeof(WorkItem) * (size_t)mi);
+  L.seg_dst = off;
+  off += align256(sizeof(int32_t) * (size_t)(nseg + 1));
   L.sorted = off;
   off += align256(sizeof(WorkItem) * (size_t)mi);
   if (is_bwd(op)) {

@@ -41,7 +41,8 @@ constexpr int kBwdBM = 64, kBwdBN = 128;
 constexpr int kF32BM = 64, kF32BN = 64;
 
 // Workspace header: status word and item count, then the per-segment item
-// offsets, the unsorted and sorted work lists, then op-specific float buffers.
+// offsets (segment order) and first slots (list order), the ordered work list,
+// then op-specific float buffers.
 struct WsHeader {
   int32_t status;
   int32_t n_items;
@@ -50,7 +51,7 @@ struct WsHeader {
 
 struct WsLayout {
   size_t seg_off;     // int32[num_seqs + 1]
-  size_t unsorted;    // WorkItem[max_items]
+  size_t seg_dst;     // int32[num_seqs]
   size_t sorted;      // WorkItem[max_items]
   size_t dvec;        // float[hq * T]      (backward: rowsum(dO * O))
   size_t dq_acc;      // float[T * hq * d]  (varlen backward only)

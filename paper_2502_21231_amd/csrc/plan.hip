@@ -6,14 +6,21 @@
 // the query tiles (forward) or key tiles (backward), counts the tiles of the
 // other side that carry visible pairs, separates the FULL ones (no score mask
 // needed) from the MASKED ones (causal diagonal or ragged key tail), and orders
-// the list by descending cost so that a grid walking it in block order starts
-// the longest tiles first (longest-processing-time-first balancing of the
-// long-tailed length mix).  Tiles with no visible pair are never listed.
+// the list so that a grid walking it in block order starts the largest work
+// first (longest-processing-time-first balancing of the long-tailed length mix)
+// while the tiles of one segment run side by side and share its K/V (forward)
+// or Q/dO (backward) tiles in L2:
+//   segments by size (len_q + len_k) descending, ties by segment index;
+//   inside a segment by descending cost, which is a closed form: a query tile
+//   sees no fewer key tiles than the one above it (forward: descending tile
+//   index), a key tile is seen by no more query tiles than the one before it
+//   (backward: ascending tile index).
+// Tiles with no visible pair are never listed.
 //
 // Three kernels, all on the caller's stream and without host synchronisation:
 //   plan_count : validate cu_seqlens, per-segment tile counts, exclusive scan
-//   plan_emit  : one thread per list entry, fills its fields
-//   plan_sort  : stable rank by (cost desc, list index asc) and scatter
+//   plan_rank  : one thread per segment: its first slot in the ordered list
+//   plan_emit  : one thread per list entry, fills its fields at its slot
 #include "common.hpp"
 
 namespace bs {
@@ -100,7 +107,8 @@ __global__ __launch_bounds__(256) void plan_emit(
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int32_t num_seqs,
     int64_t total_q, int64_t total_k, int32_t diag_chunk, int causal, int kind, int tile_a,
     int tile_b, int64_t max_items, const WsHeader* __restrict__ hdr,
-    const int32_t* __restrict__ seg_off, WorkItem* __restrict__ items) {
+    const int32_t* __restrict__ seg_off, const int32_t* __restrict__ seg_dst,
+    WorkItem* __restrict__ items) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= max_items || i >= hdr->n_items) return;
   const int32_t nseg = cu_q == nullptr ? 1 : num_seqs;
@@ -138,7 +146,7 @@ __global__ __launch_bounds__(256) void plan_emit(
     w.b_len = (int32_t)s.lk;
     w.n0 = (int32_t)n_full;
     w.n1 = (int32_t)n_tiles;
-    w.n2 = (int32_t)n_tiles;  // sort key
+    w.n2 = (int32_t)n_tiles;
   } else {
     const int64_t BM = tile_b, BN = tile_a;
     const int64_t k_first = tile * BN;
@@ -169,35 +177,44 @@ __global__ __launch_bounds__(256) void plan_emit(
     w.n1 = (int32_t)n_masked;
     w.n2 = (int32_t)n_vis;
   }
-  items[i] = w;
+  const int64_t cnt = seg_off[b + 1] - seg_off[b];
+  items[seg_dst[b] + (kind == kPlanFwd ? cnt - 1 - tile : tile)] = w;
 }
 
-// Sort key of an unsorted entry: forward n_tiles, backward n_vis (both in n2).
-constexpr int kSortChunk = 1024;
+// First slot of each segment in the ordered list: the items of every segment that
+// comes before it (larger len_q + len_k, or equal size and a lower index).
+constexpr int kRankChunk = 1024;
 
-__global__ __launch_bounds__(256) void plan_sort(int64_t max_items,
+__global__ __launch_bounds__(256) void plan_rank(const int32_t* __restrict__ cu_q,
+                                                 const int32_t* __restrict__ cu_k, int32_t num_seqs,
                                                  const WsHeader* __restrict__ hdr,
-                                                 const WorkItem* __restrict__ in,
-                                                 WorkItem* __restrict__ out) {
-  __shared__ int32_t keys[kSortChunk];
-  const int64_t n = hdr->n_items;
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if ((int64_t)blockIdx.x * blockDim.x >= n) return;  // whole block idle (uniform)
-  const bool live = i < n && i < max_items;
-  const int32_t mine = live ? in[i].n2 : 0;
-  int64_t rank = 0;
-  for (int64_t base = 0; base < n; base += kSortChunk) {
-    for (int j = threadIdx.x; j < kSortChunk; j += blockDim.x)
-      keys[j] = base + j < n ? in[base + j].n2 : -1;
+                                                 const int32_t* __restrict__ seg_off,
+                                                 int32_t* __restrict__ seg_dst) {
+  __shared__ int64_t ssz[kRankChunk];
+  __shared__ int32_t scnt[kRankChunk];
+  if (hdr->status != 0) return;  // uniform: the list is empty
+  const int32_t nseg = cu_q == nullptr ? 1 : num_seqs;
+  const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
+  auto size_of = [&](int32_t x) -> int64_t {
+    return cu_q == nullptr ? 0 : ((int64_t)cu_q[x + 1] - cu_q[x]) + ((int64_t)cu_k[x + 1] - cu_k[x]);
+  };
+  const int64_t mine = b < nseg ? size_of(b) : 0;
+  int64_t dst = 0;
+  for (int32_t base = 0; base < nseg; base += kRankChunk) {
+    for (int j = threadIdx.x; j < kRankChunk; j += blockDim.x) {
+      const bool ok = base + j < nseg;
+      ssz[j] = ok ? size_of(base + j) : 0;
+      scnt[j] = ok ? seg_off[base + j + 1] - seg_off[base + j] : 0;
+    }
     __syncthreads();
-    const int64_t lim = n - base < kSortChunk ? n - base : kSortChunk;
-    for (int64_t j = 0; j < lim; ++j) {
-      const int32_t kj = keys[j];
-      rank += (kj > mine) || (kj == mine && base + j < i);
+    const int32_t lim = nseg - base < kRankChunk ? nseg - base : kRankChunk;
+    for (int32_t j = 0; j < lim; ++j) {
+      const bool before = ssz[j] > mine || (ssz[j] == mine && base + j < b);
+      dst += before ? scnt[j] : 0;
     }
     __syncthreads();
   }
-  if (live) out[rank] = in[i];
+  if (b < nseg) seg_dst[b] = (int32_t)dst;
 }
 
 }  // namespace
@@ -209,17 +226,18 @@ hipError_t launch_plan(PlanKind kind, const int32_t* cu_q, const int32_t* cu_k, 
   char* base = static_cast<char*>(ws);
   WsHeader* hdr = reinterpret_cast<WsHeader*>(base);
   int32_t* seg_off = reinterpret_cast<int32_t*>(base + L.seg_off);
-  WorkItem* unsorted = reinterpret_cast<WorkItem*>(base + L.unsorted);
+  int32_t* seg_dst = reinterpret_cast<int32_t*>(base + L.seg_dst);
   WorkItem* sorted = reinterpret_cast<WorkItem*>(base + L.sorted);
   hipLaunchKernelGGL(plan_count, dim3(1), dim3(kCountThreads), 0, stream, cu_q, cu_k, num_seqs,
                      total_q, total_k, max_seqlen, (int)kind, tile_a, hdr, seg_off);
   if (max_items > 0) {
+    const int32_t nseg = cu_q == nullptr ? 1 : num_seqs;
+    hipLaunchKernelGGL(plan_rank, dim3((unsigned)((nseg + 255) / 256)), dim3(256), 0, stream, cu_q,
+                       cu_k, num_seqs, hdr, seg_off, seg_dst);
     const unsigned blocks = (unsigned)((max_items + 255) / 256);
     hipLaunchKernelGGL(plan_emit, dim3(blocks), dim3(256), 0, stream, cu_q, cu_k, num_seqs,
                        total_q, total_k, diag_chunk, causal, (int)kind, tile_a, tile_b,
-                       max_items, hdr, seg_off, unsorted);
-    hipLaunchKernelGGL(plan_sort, dim3(blocks), dim3(256), 0, stream, max_items, hdr, unsorted,
-                       sorted);
+                       max_items, hdr, seg_off, seg_dst, sorted);
   }
   return hipGetLastError();
 }

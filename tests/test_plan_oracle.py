@@ -49,13 +49,29 @@ def test_work_list_covers_exactly_the_visible_pairs(kind):
         assert covered == sum(l * (l + 1) // 2 for l in lens)
 
 
-def test_order_is_cost_descending_with_index_tiebreak():
-    lens = [300, 5, 64, 64, 1000]
+@pytest.mark.parametrize("kind", ["fwd", "bwd"])
+@pytest.mark.parametrize("causal", [True, False])
+def test_order_groups_segments_largest_first_with_cost_descending_inside(kind, causal):
+    # segments of equal size (64, 64) keep index order; every segment's tiles are
+    # contiguous; inside a segment the tile order is the closed form (forward
+    # descending, backward ascending index) and must be non-increasing cost
+    lens = [300, 5, 64, 64, 1000, 0, 129]
     cu = np.concatenate([[0], np.cumsum(lens)])
-    items = P.varlen_plan(cu, cu, True, 64, 32, "fwd")
-    keys = [(-it[7], it[0], it[1]) for it in items]
-    assert keys == sorted(keys)
-    assert len(items) == sum((l + 63) // 64 for l in lens)
+    BM, BN = (64, 32) if kind == "fwd" else (32, 64)
+    items = P.varlen_plan(cu, cu, causal, BM, BN, kind)
+    segs = [it[0] for it in items]
+    runs = [s for i, s in enumerate(segs) if i == 0 or segs[i - 1] != s]
+    assert len(runs) == len(set(runs)), "a segment's tiles are not contiguous"
+    assert runs == sorted(runs, key=lambda b: (-2 * lens[b], b))
+    cost = 7 if kind == "fwd" else 8
+    for b in runs:
+        mine = [it for it in items if it[0] == b]
+        tiles = [it[1] for it in mine]
+        assert tiles == (sorted(tiles, reverse=True) if kind == "fwd" else sorted(tiles))
+        costs = [it[cost] for it in mine]
+        assert costs == sorted(costs, reverse=True)
+    tile = BM if kind == "fwd" else BN  # query tiles (forward) or key tiles (backward)
+    assert len(items) == sum((l + tile - 1) // tile for l in lens)
 
 
 def test_chunk_plan_past_diagonal_and_future():

@@ -17,11 +17,12 @@
 //   over 64-row query tiles).  8 waves, 2 per SIMD, in pairs: both waves of
 //   pair b own the 32-key block b of the tile, and split the work by role.
 //     S wave  (holds K of its keys): S = Q K^T, P = exp2(S*c - LSE*log2e)
-//                                    (lane = one key, 64 query rows), hands P
-//                                    to its partner through LDS (fp32), and
-//                                    accumulates dV^T += dO^T P.
-//     dP wave (holds V of its keys): dP = dO V^T, dS = P (dP - D) with the P
-//                                    of its partner, dK^T += Q^T dS.
+//                                    (lane = one key, 64 query rows), hands the
+//                                    bf16 P that feeds its own products to its
+//                                    partner through LDS, and accumulates
+//                                    dV^T += dO^T P.
+//     dP wave (holds V of its keys): dP = dO V^T, dS = P (dP - D) with that
+//                                    bf16 P, dK^T += Q^T dS.
 //   Row operands (Q for S, dO for dP) are row reads of the query tiles, the
 //   transposed ones (dO^T, Q^T) transposing LDS reads of the same tiles; P and
 //   dS feed the MFMA straight from registers.  Each wave keeps only one of the
@@ -232,8 +233,8 @@ void dkdv_bf16_kernel(const BwdParams p) {
   // LSE (log2 units) then D rows of the query tile, double-buffered
   __shared__ __attribute__((aligned(16))) float R0[2 * BM];
   __shared__ __attribute__((aligned(16))) float R1[2 * BM];
-  // P handed from the S wave to the dP wave of each key block: [block][vector][lane]
-  __shared__ __attribute__((aligned(16))) f32x4 Ps[4 * MB * 4 * 64];
+  // bf16 P handed from the S wave to the dP wave of each key block: [block][step][lane]
+  __shared__ __attribute__((aligned(16))) bf16x8 Ps[4 * QS * 64];
 
   const int item_idx = blockIdx.x / p.hkv;
   if (item_idx >= p.hdr->n_items) return;
@@ -307,7 +308,7 @@ void dkdv_bf16_kernel(const BwdParams p) {
   // phase 1 reads rows of Q (role 0) or dO (role 1); phase 2 reads dO (role 0)
   // or Q (role 1) transposed
   const int base1 = role * QTILE, base2 = (1 - role) * QTILE;
-  f32x4* pslot = Ps + kb * (MB * 4) * 64 + lane;
+  bf16x8* pslot = Ps + kb * QS * 64 + lane;
 
   // one query tile: consume (QDb, Rb) while tile i+1 is copied into (QDn, Rn),
   // which were last read one tile earlier, before the barrier that ended it
@@ -356,16 +357,13 @@ void dkdv_bf16_kernel(const BwdParams p) {
 #pragma unroll
           for (int a4 = 0; a4 < 4; ++a4) {
             const f32x4 l4 = *reinterpret_cast<const f32x4*>(&Rb[mb * 32 + a4 * 8 + hh * 4]);
-            f32x4 pv;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const int r = a4 * 4 + e;
               float pr = fast_exp2(fmaf(s[mb][r], p.scale_log2, -l4[e]));
               if (decltype(use_mask)::value) pr = (mb * 32 + a4 * 8 + e) >= vis_lim ? pr : 0.f;
-              pv[e] = pr;
               ob[mb * 2 + (r >> 3)][r & 7] = f2bf(pr);
             }
-            pslot[(mb * 4 + a4) * 64] = pv;
           }
         }
       };
@@ -373,19 +371,22 @@ void dkdv_bf16_kernel(const BwdParams p) {
         softmax(std::true_type{});
       else
         softmax(std::false_type{});
+#pragma unroll
+      for (int qs = 0; qs < QS; ++qs) pslot[qs * 64] = ob[qs];  // the bf16 P that feeds dV
     }
     barrier_lds();  // P of every key block is in LDS (the copies of tile i+1 stay in flight)
     if (role == 1) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
+        const bf16x8 p0 = pslot[(mb * 2) * 64], p1 = pslot[(mb * 2 + 1) * 64];
 #pragma unroll
         for (int a4 = 0; a4 < 4; ++a4) {
           const f32x4 d4 = *reinterpret_cast<const f32x4*>(&Rb[BM + mb * 32 + a4 * 8 + hh * 4]);
-          const f32x4 pv = pslot[(mb * 4 + a4) * 64];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int r = a4 * 4 + e;
-            ob[mb * 2 + (r >> 3)][r & 7] = f2bf(pv[e] * (s[mb][r] - d4[e]));
+            const float pr = bf2f((r >> 3) == 0 ? p0[r & 7] : p1[r & 7]);
+            ob[mb * 2 + (r >> 3)][r & 7] = f2bf(pr * (s[mb][r] - d4[e]));
           }
         }
       }

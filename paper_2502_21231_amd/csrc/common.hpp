@@ -147,33 +147,52 @@ __device__ __forceinline__ int swz_off(int r, int c) {
 
 // One wave's share of copying rows 0..R-1 of a swizzled [R][D] bf16 tile from global
 // memory straight into LDS (buffer_load_dwordx4 ... lds: lane l of an instruction
-// writes 16 bytes at LDS base + 16*l, so an instruction fills 64/(D/8) whole rows and
-// each lane fetches the global chunk that the swizzle places at its LDS position).
-// Row r of the tile comes from src + min(r, last) * gstride elements: rows past the
-// end repeat the last valid one.  Completion is waited for with wait_vmem_all().
+// writes 16 bytes at LDS base + offset + 16*l, so an instruction fills 64/(D/8) whole
+// rows, 1 KB, and each lane fetches the global chunk that the swizzle places at its
+// LDS position).  Row r of the tile comes from src + min(r, last) * gstride elements:
+// rows past the end repeat the last valid one.  Completion is waited for with
+// wait_vmem_all().
+//
+// Each wave copies a contiguous run of PER instructions from one LDS base (M0): the
+// instruction offset (0, 1 KB, 2 KB, 3 KB) moves both the LDS and the global address,
+// so the per-lane global offsets subtract it, and the buffer starts 4 KB before `src`
+// to keep them non-negative (only src + row offsets are ever accessed).
 //
 // The buffer form (MUBUF) rather than global_load_lds (FLAT): the compiler treats a
 // pending FLAT copy into LDS as a possible LDS access of unknown order and then
 // waits for all LDS reads (lgkmcnt(0)) before every use, which defeats reading LDS
-// operands ahead.  The buffer is the tile's rows from `src`; byte offsets
-// (R rows x gstride x 2) stay below 2^31 for the head counts the C API accepts.
+// operands ahead.  Byte offsets (R rows x gstride x 2 + 4 KB) stay below 2^31 for
+// the head counts the C API accepts.
+template <int K, int PER, int D>
+struct DmaRun {
+  static __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, bf16* lds, int row0,
+                                               int sub, int phys, int gstride, int last) {
+    constexpr int RPI = 64 / (D / 8);
+    const int row = row0 + K * RPI + sub;
+    const int r = row < last ? row : last;
+    const int voff = (r * gstride + ((phys ^ swz_g<D>(row)) << 3)) * 2 + 4096 - K * 1024;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16,
+                                             voff, 0, K * 1024, 0);
+    DmaRun<K + 1, PER, D>::issue(rs, lds, row0, sub, phys, gstride, last);
+  }
+};
+template <int PER, int D>
+struct DmaRun<PER, PER, D> {
+  static __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t, bf16*, int, int, int, int,
+                                               int) {}
+};
+
 template <int D, int R, int NWAVES>
 __device__ __forceinline__ void dma_tile(bf16* lds_tile, const bf16* src, int gstride, int last,
                                          int wave, int lane) {
-  constexpr int CPR = D / 8, RPI = 64 / CPR, NI = R / RPI;
+  constexpr int CPR = D / 8, RPI = 64 / CPR, NI = R / RPI, PER = NI / NWAVES;
   static_assert(NI % NWAVES == 0, "whole instructions per wave");
+  static_assert(PER >= 1 && PER <= 4, "instruction offsets of one run fit in 12 bits");
   const int sub = lane / CPR, phys = lane % CPR;
-  const __amdgpu_buffer_rsrc_t rsrc =
-      __builtin_amdgcn_make_buffer_rsrc((void*)src, 0, 0x7fffffff, 0x00020000);
-#pragma unroll
-  for (int k = 0; k < NI / NWAVES; ++k) {
-    const int u = k * NWAVES + wave;
-    const int row = u * RPI + sub;
-    const int r = row < last ? row : last;
-    const int voff = (r * gstride + ((phys ^ swz_g<D>(row)) << 3)) * 2;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(lds_tile + u * RPI * D),
-                                             16, voff, 0, 0, 0);
-  }
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(reinterpret_cast<const char*>(src) - 4096), 0, 0x7fffffff, 0x00020000);
+  const int u0 = wave * PER;  // first instruction (1 KB of LDS) of this wave's run
+  DmaRun<0, PER, D>::issue(rsrc, lds_tile + u0 * RPI * D, u0 * RPI, sub, phys, gstride, last);
 }
 
 // Element offset, in a swizzled tile, of this lane's 8-byte piece of the transposing

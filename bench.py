@@ -130,6 +130,8 @@ def run_varlen_bench(args, dev):
                      "head_dim": d, "segments": nseq, "seed": args.seed, "visible_pairs": A,
                      "longest_segment": maxlen}
     res["flops_per_step"] = flops_fwd + flops_bwd
+    # causal counted as half of each segment's s^2: A - T/2 pairs
+    res["value_half_s2"] = res["value"] * (A - T / 2) / A
     if args.cpu_baseline:
         res["cpu_baseline"] = cpu_baseline_varlen(W, scale)
     return res
@@ -142,17 +144,20 @@ def time_steps(step, args, dev, flops_fwd, flops_bwd):
         step()
     torch.cuda.synchronize(dev)
     s = torch.cuda.current_stream(dev)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     B.bs_set_profiling(True)
     torch.cuda.synchronize(dev)
-    e0.record(s)
+    ev[0].record(s)
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
         step()
-    e1.record(s)
+        ev[i + 1].record(s)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
-    total_ms = e0.elapsed_time(e1)
+    total_ms = ev[0].elapsed_time(ev[-1])
+    per_step = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
+    median_ms = per_step[len(per_step) // 2] if len(per_step) % 2 else \
+        0.5 * (per_step[len(per_step) // 2 - 1] + per_step[len(per_step) // 2])
     kern = {}
     names = {B.BS_KERNEL_PLAN: "plan", B.BS_KERNEL_FWD: "fwd", B.BS_KERNEL_PREPROCESS: "bwd_preprocess",
              B.BS_KERNEL_BWD_DQ: "bwd_dq", B.BS_KERNEL_BWD_DKDV: "bwd_dkdv",
@@ -176,7 +181,7 @@ def time_steps(step, args, dev, flops_fwd, flops_bwd):
     dom_launches = kern[dom]["launches_per_step"]
     achieved = dom_flops / dom_launches / (kern[dom]["avg_ms_per_launch"] * 1e-3) / 1e12
     return {
-        "value": value, "ms_per_step": ms_step, "wall_s": wall,
+        "value": value, "ms_per_step": ms_step, "ms_per_step_median": median_ms, "wall_s": wall,
         "pct_of_bf16_peak": 100.0 * value / BF16_PEAK_TFLOPS,
         "fwd_tflops": flops_fwd / (fwd_ms * 1e-3) / 1e12 if fwd_ms == fwd_ms else None,
         "bwd_tflops": flops_bwd / (bwd_ms * 1e-3) / 1e12 if bwd_ms == bwd_ms else None,
@@ -296,6 +301,9 @@ def run_chunk_bench(args, dev):
                      "heads_kv": hkv, "head_dim": d, "q_offsets": q_offs, "kv_offsets": kv_offs,
                      "pairs": pairs, "seed": seed, "visible_pairs": A}
     res["flops_per_step"] = flops_fwd + flops_bwd
+    # causal counted as half of c^2 for each diagonal chunk pair (c(c+1)/2 exact)
+    n_diag = sum(1 for i, j in pairs if q_offs[i] == kv_offs[j])
+    res["value_half_s2"] = res["value"] * (A - n_diag * c / 2) / A
     merge = res["kernels"].get("lse_merge")
     if merge:
         # algorithmic bytes of one merge of n partials: read n O and LSE rows, write one of each
@@ -359,10 +367,14 @@ def main():
     line = {
         "metric": "attention fwd+bwd TFLOP/s (causal-adjusted) and % of bf16 MFMA peak, 1 GPU",
         "value": round(res["value"], 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(res["ms_per_step"], 4), "higher_is_better": True,
+        "warmup": args.warmup, "ms_per_step": round(res["ms_per_step"], 4),
+        "ms_per_step_median": round(res["ms_per_step_median"], 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": res["config"],
         "pct_of_bf16_peak": round(res["pct_of_bf16_peak"], 2),
+        # the same FLOPs counted the common way for causal attention (half of the dense S^2 per
+        # segment): 0.5 * 14 d Hq sum(s^2) instead of 14 d Hq A with A = sum s(s+1)/2
+        "value_half_s2_convention": res.get("value_half_s2"),
         "fwd_tflops": res["fwd_tflops"], "bwd_tflops": res["bwd_tflops"],
         "kernels": res["kernels"], "flops_per_step": res["flops_per_step"],
         "roofline": res["roofline"],

@@ -88,7 +88,9 @@ enum {
   BS_OP_VARLEN_FWD = 0,
   BS_OP_VARLEN_BWD = 1,
   BS_OP_CHUNK_FWD = 2,
-  BS_OP_CHUNK_BWD = 3
+  BS_OP_CHUNK_BWD = 3,
+  BS_OP_PACKED_CHUNK_FWD = 4,
+  BS_OP_PACKED_CHUNK_BWD = 5
 };
 
 /* Device status word values (bs_read_device_status). */
@@ -101,7 +103,7 @@ enum {
 };
 
 /* Bytes of workspace that `op` needs for these sizes (num_seqs, max_seqlen are
- * ignored by the chunk ops).  Returns 0 when the arguments are invalid (then
+ * ignored by the two single-chunk ops).  Returns 0 when the arguments are invalid (then
  * bs_last_error() says why).  The workspace needs no initialisation and holds
  * nothing across calls except what bs_read_device_status() reads. */
 size_t bs_attn_workspace_size(int op, const bs_dims* dims, int32_t num_seqs, int32_t max_seqlen);
@@ -155,6 +157,42 @@ int bs_attn_chunk_bwd(const bs_dims* dims, const void* q, const void* k, const v
                       float* dq_accum, void* dk, void* dv, int kv_accumulate, void* workspace,
                       size_t workspace_bytes, void* stream);
 
+/* Packed context-parallel step (Sec. 7, Dist-attn with packing: every
+ * subsequence of a packed micro-batch is split into 2N parts, device i holds
+ * parts i and 2N-1-i of each, and the ring passes the KV parts around).  One call
+ * covers the part pairs of many subsequences: segment b holds queries
+ * cu_seqlens_q[b] .. cu_seqlens_q[b+1]-1 whose first token sits at global
+ * position q_pos[b] of its subsequence, and keys cu_seqlens_k[b] ..
+ * cu_seqlens_k[b+1]-1 whose first token sits at k_pos[b] (cu_seqlens: int32,
+ * num_seqs+1 entries, validated as for the varlen ops; q_pos, k_pos: int64 device
+ * arrays of num_seqs entries).  With causal != 0 key j of segment b is visible to
+ * query i iff k_pos[b] + j <= q_pos[b] + i.  Empty segments, and segments whose
+ * keys are all in the future, are legal.  Writes this step's partial out
+ * [T, hq, d] and lse [hq, T] with the conventions of bs_attn_chunk_fwd (rows that
+ * see no key: out = 0, lse = -inf); combine the partials with bs_lse_merge().
+ * A zig-zag ring step is two calls: the "straight" pairs (query part i with key
+ * part j, part 2N-1-i with part 2N-1-j) and the "crossed" ones (part i with part
+ * 2N-1-j, part 2N-1-i with part j, the key buffer holding the parts in that
+ * order). */
+int bs_attn_packed_chunk_fwd(const bs_dims* dims, const void* q, const void* k, const void* v,
+                             const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                             const int64_t* q_pos, const int64_t* k_pos, int32_t num_seqs,
+                             int32_t max_seqlen, int causal, float scale, void* out, float* lse,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward of one packed context-parallel step, with the conventions of
+ * bs_attn_chunk_bwd: out_merged / lse_merged are the final forward results of
+ * these query rows, this step's dQ is added into dq_accum (float32 [T, hq, d]),
+ * and dk, dv are overwritten (kv_accumulate == 0) or float32 accumulators
+ * (kv_accumulate != 0).  Each key row belongs to one segment of the call. */
+int bs_attn_packed_chunk_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,
+                             const void* out_merged, const float* lse_merged, const void* dout,
+                             const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                             const int64_t* q_pos, const int64_t* k_pos, int32_t num_seqs,
+                             int32_t max_seqlen, int causal, float scale, float* dq_accum,
+                             void* dk, void* dv, int kv_accumulate, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
 /* Rounds a float32 dQ accumulator [T, hq, d] into dq of dims->dtype (RNE). */
 int bs_dq_finalize(const bs_dims* dims, const float* dq_accum, void* dq, void* stream);
 
@@ -179,14 +217,15 @@ int bs_read_device_status(const void* workspace, void* stream);
  * item count and tile_m / tile_n (may be NULL) the tile sizes it used.
  * Forward items: seg, qtile, q_start, q_rows, k_start, k_len, n_full, n_tiles,
  * diag, 0, 0, 0.  Backward items: seg, ktile, k_start, k_rows, q_start, q_len,
- * qt_first, n_masked, n_vis, diag, 0, 0.  For the chunk ops cu_seqlens are
- * ignored and the offsets are used. */
+ * qt_first, n_masked, n_vis, diag, 0, 0.  For the single-chunk ops cu_seqlens
+ * are ignored and q_pos_offset / k_pos_offset are used; the packed chunk ops use
+ * cu_seqlens and the per-segment device arrays q_pos / k_pos (NULL otherwise). */
 int bs_attn_plan_export(int op, const bs_dims* dims, const int32_t* cu_seqlens_q,
                         const int32_t* cu_seqlens_k, int32_t num_seqs, int32_t max_seqlen,
-                        int64_t q_pos_offset, int64_t k_pos_offset, int causal,
-                        void* workspace, size_t workspace_bytes, int32_t* host_items,
-                        size_t capacity, size_t* count, int32_t* tile_m, int32_t* tile_n,
-                        void* stream);
+                        int64_t q_pos_offset, int64_t k_pos_offset, const int64_t* q_pos,
+                        const int64_t* k_pos, int causal, void* workspace,
+                        size_t workspace_bytes, int32_t* host_items, size_t capacity,
+                        size_t* count, int32_t* tile_m, int32_t* tile_n, void* stream);
 
 /* Kernel classes timed by the profiling hooks below. */
 enum {

@@ -24,7 +24,10 @@ Readings where the paper is silent (no attention formula is printed):
     a partial weight 0;
   * in varlen mode with len_q != len_k the causal diagonal is aligned
     bottom-right (key j visible to query i iff j <= i + len_k - len_q);
-  * in chunk mode key j is visible to query i iff k_off + j <= q_off + i.
+  * in chunk mode key j is visible to query i iff k_off + j <= q_off + i;
+  * a packed chunk step (Sec. 7, Dist-attn with packing: the 2N parts of many
+    subsequences in one buffer) is a list of segments, each with the global
+    positions of its first query and first key, and the chunk rule per segment.
 
 Rows are processed in blocks of query rows only to bound memory: the
 arithmetic of every row is exactly the unblocked definition.
@@ -123,6 +126,25 @@ def chunk_fwd(q, k, v, q_off: int, k_off: int, causal: bool, scale: float):
     return _segment_fwd(q, k, v, scale, int(q_off) - int(k_off), causal, hq, hkv)
 
 
+def packed_chunk_fwd(q, k, v, cu_q, cu_k, q_pos, k_pos, causal: bool, scale: float):
+    """One packed context-parallel step: segment b pairs query rows cu_q[b]..cu_q[b+1]-1, whose
+    first token sits at global position q_pos[b], with key rows cu_k[b]..cu_k[b+1]-1 starting at
+    k_pos[b]; key j is visible to query i iff k_pos[b] + j <= q_pos[b] + i.  Returns the partial
+    O [T, Hq, d] and LSE [Hq, T] (rows that see no key: O = 0, LSE = -inf)."""
+    q, k, v = _as64(q), _as64(k), _as64(v)
+    cu_q, cu_k = np.asarray(cu_q, np.int64), np.asarray(cu_k, np.int64)
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    o = np.zeros((T, hq, d))
+    lse = np.full((hq, T), -np.inf)
+    for b in range(len(cu_q) - 1):
+        q0, q1, k0, k1 = cu_q[b], cu_q[b + 1], cu_k[b], cu_k[b + 1]
+        diag = int(q_pos[b]) - int(k_pos[b])
+        ob, lb = _segment_fwd(q[q0:q1], k[k0:k1], v[k0:k1], scale, diag, causal, hq, hkv)
+        o[q0:q1], lse[:, q0:q1] = ob, lb
+    return o, lse
+
+
 def lse_merge(o_parts, lse_parts):
     """Combine partials of the same queries over disjoint key sets.
 
@@ -198,6 +220,23 @@ def chunk_bwd(q, k, v, o_merged, lse_merged, do, q_off: int, k_off: int, causal:
     q, k, v, o, lse, do = (_as64(x) for x in (q, k, v, o_merged, lse_merged, do))
     hq, hkv = q.shape[1], k.shape[1]
     return _segment_bwd(q, k, v, o, lse, do, scale, int(q_off) - int(k_off), causal, hq, hkv)
+
+
+def packed_chunk_bwd(q, k, v, o_merged, lse_merged, do, cu_q, cu_k, q_pos, k_pos, causal: bool,
+                     scale: float):
+    """Backward of one packed context-parallel step with the merged O and LSE of the query rows:
+    this step's dQ contribution [T,Hq,d] and the dK, dV [Tk,Hkv,d] of its key rows."""
+    q, k, v, o, lse, do = (_as64(x) for x in (q, k, v, o_merged, lse_merged, do))
+    cu_q, cu_k = np.asarray(cu_q, np.int64), np.asarray(cu_k, np.int64)
+    hq, hkv = q.shape[1], k.shape[1]
+    dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    for b in range(len(cu_q) - 1):
+        q0, q1, k0, k1 = cu_q[b], cu_q[b + 1], cu_k[b], cu_k[b + 1]
+        diag = int(q_pos[b]) - int(k_pos[b])
+        a, bb, c = _segment_bwd(q[q0:q1], k[k0:k1], v[k0:k1], o[q0:q1], lse[:, q0:q1],
+                                do[q0:q1], scale, diag, causal, hq, hkv)
+        dq[q0:q1], dk[k0:k1], dv[k0:k1] = a, bb, c
+    return dq, dk, dv
 
 
 def visible_pairs(len_q: int, len_k: int, diag: int, causal: bool) -> int:

@@ -130,6 +130,20 @@ def varlen_plan(cu_q, cu_k, causal, BM, BN, kind="fwd"):
     return _order(items, kind, size)
 
 
+def packed_plan(cu_q, cu_k, q_pos, k_pos, causal, BM, BN, kind="fwd"):
+    """Ordered work list of a packed context-parallel step: segment b is a chunk pair whose
+    first query and key sit at global positions q_pos[b], k_pos[b] (diag = q_pos - k_pos)."""
+    items, size = [], {}
+    for b, q0, lq, k0, lk in _segments(cu_q, cu_k):
+        diag = int(q_pos[b]) - int(k_pos[b])
+        size[b] = lq + lk
+        if kind == "fwd":
+            items += fwd_items_for_segment(b, q0, lq, k0, lk, diag, causal, BM, BN)
+        else:
+            items += bwd_items_for_segment(b, q0, lq, k0, lk, diag, causal, BM, BN)
+    return _order(items, kind, size)
+
+
 def chunk_plan(len_q, len_k, q_off, k_off, causal, BM, BN, kind="fwd"):
     """Ordered work list of one context-parallel chunk pair (a single segment)."""
     diag = int(q_off) - int(k_off)

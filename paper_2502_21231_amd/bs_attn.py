@@ -19,11 +19,13 @@ LIB_PATH = os.path.join(_HERE, "libbs_attn.so")
 
 BS_OK, BS_ERR_INVALID_ARG, BS_ERR_UNSUPPORTED, BS_ERR_WORKSPACE, BS_ERR_HIP, BS_ERR_DEVICE_STATUS = range(6)
 BS_F32, BS_BF16 = 0, 1
-BS_OP_VARLEN_FWD, BS_OP_VARLEN_BWD, BS_OP_CHUNK_FWD, BS_OP_CHUNK_BWD = range(4)
+(BS_OP_VARLEN_FWD, BS_OP_VARLEN_BWD, BS_OP_CHUNK_FWD, BS_OP_CHUNK_BWD, BS_OP_PACKED_CHUNK_FWD,
+ BS_OP_PACKED_CHUNK_BWD) = range(6)
 
 EXPORTS = (
     "bs_attn_workspace_size", "bs_attn_varlen_fwd", "bs_attn_varlen_bwd", "bs_attn_chunk_fwd",
-    "bs_attn_chunk_bwd", "bs_dq_finalize", "bs_lse_merge", "bs_read_device_status",
+    "bs_attn_chunk_bwd", "bs_attn_packed_chunk_fwd", "bs_attn_packed_chunk_bwd",
+    "bs_dq_finalize", "bs_lse_merge", "bs_read_device_status",
     "bs_attn_plan_export", "bs_set_profiling", "bs_profile_read", "bs_last_error",
 )
 (BS_KERNEL_PLAN, BS_KERNEL_FWD, BS_KERNEL_PREPROCESS, BS_KERNEL_BWD_DQ, BS_KERNEL_BWD_DKDV,
@@ -65,11 +67,16 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                              _P, _SZ, _P]),
         "bs_attn_chunk_bwd": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _I64, _I64, ctypes.c_int,
                                              _F, _P, _P, _P, ctypes.c_int, _P, _SZ, _P]),
+        "bs_attn_packed_chunk_fwd": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _P, _I32, _I32,
+                                                    ctypes.c_int, _F, _P, _P, _P, _SZ, _P]),
+        "bs_attn_packed_chunk_bwd": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                                    _I32, _I32, ctypes.c_int, _F, _P, _P, _P,
+                                                    ctypes.c_int, _P, _SZ, _P]),
         "bs_dq_finalize": (ctypes.c_int, [_DIMS, _P, _P, _P]),
         "bs_lse_merge": (ctypes.c_int, [_DIMS, _P, _P, _I32, _P, _P, _P]),
         "bs_read_device_status": (ctypes.c_int, [_P, _P]),
         "bs_attn_plan_export": (ctypes.c_int, [ctypes.c_int, _DIMS, _P, _P, _I32, _I32, _I64, _I64,
-                                               ctypes.c_int, _P, _SZ, _P, _SZ,
+                                               _P, _P, ctypes.c_int, _P, _SZ, _P, _SZ,
                                                ctypes.POINTER(_SZ), ctypes.POINTER(_I32),
                                                ctypes.POINTER(_I32), _P]),
         "bs_set_profiling": (ctypes.c_int, [ctypes.c_int]),
@@ -252,6 +259,72 @@ def bs_attn_chunk_bwd(q, k, v, out_merged, lse_merged, dout, q_pos_offset: int, 
     return dq_accum, dk, dv
 
 
+def _segments(cu_seqlens_q, cu_seqlens_k, q_pos, k_pos):
+    _need(cu_seqlens_q, "cu_seqlens_q", torch.int32, 1)
+    _need(cu_seqlens_k, "cu_seqlens_k", torch.int32, 1)
+    _need(q_pos, "q_pos", torch.int64, 1)
+    _need(k_pos, "k_pos", torch.int64, 1)
+    nseq = cu_seqlens_q.numel() - 1
+    if cu_seqlens_k.numel() != nseq + 1 or q_pos.numel() != nseq or k_pos.numel() != nseq:
+        raise ValueError("cu_seqlens_q/k need num_seqs+1 entries and q_pos/k_pos num_seqs")
+    return nseq
+
+
+def bs_attn_packed_chunk_fwd(q, k, v, cu_seqlens_q, cu_seqlens_k, q_pos, k_pos, max_seqlen: int,
+                             causal: bool = True, scale: float | None = None, out=None, lse=None,
+                             workspace=None):
+    """One packed context-parallel step over many segments: segment b pairs query rows
+    cu_seqlens_q[b]..cu_seqlens_q[b+1]-1 at global positions q_pos[b]+i with key rows
+    cu_seqlens_k[b].. at k_pos[b]+j (int32 / int64 device tensors).  Returns the partial
+    (out, lse)."""
+    _qkv(q, k, v)
+    nseq = _segments(cu_seqlens_q, cu_seqlens_k, q_pos, k_pos)
+    dims = make_dims(q, k)
+    out = torch.empty_like(q) if out is None else out
+    lse = torch.empty(q.shape[1], q.shape[0], dtype=torch.float32, device=q.device) if lse is None else lse
+    _need(out, "out", q.dtype)
+    _need(lse, "lse", torch.float32)
+    if workspace is None:
+        workspace = alloc_workspace(BS_OP_PACKED_CHUNK_FWD, dims, q.device, nseq, max_seqlen)
+    _check(load_library().bs_attn_packed_chunk_fwd(
+        ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_q), _ptr(cu_seqlens_k),
+        _ptr(q_pos), _ptr(k_pos), nseq, int(max_seqlen), int(bool(causal)), _scale(scale, q.shape[2]),
+        _ptr(out), _ptr(lse), _ptr(workspace), workspace.numel(), _stream(q.device)))
+    return out, lse
+
+
+def bs_attn_packed_chunk_bwd(q, k, v, out_merged, lse_merged, dout, cu_seqlens_q, cu_seqlens_k,
+                             q_pos, k_pos, max_seqlen: int, causal: bool = True,
+                             scale: float | None = None, dq_accum=None, dk=None, dv=None,
+                             kv_accumulate: bool = False, workspace=None):
+    """Backward of one packed context-parallel step, with the conventions of
+    bs_attn_chunk_bwd; returns (dq_accum, dk, dv)."""
+    _qkv(q, k, v)
+    _need(out_merged, "out_merged", q.dtype)
+    _need(dout, "dout", q.dtype)
+    _need(lse_merged, "lse_merged", torch.float32)
+    nseq = _segments(cu_seqlens_q, cu_seqlens_k, q_pos, k_pos)
+    dims = make_dims(q, k)
+    if dq_accum is None:
+        dq_accum = torch.zeros(q.shape, dtype=torch.float32, device=q.device)
+    _need(dq_accum, "dq_accum", torch.float32)
+    kv_dtype = torch.float32 if kv_accumulate else k.dtype
+    if dk is None:
+        dk = torch.zeros(k.shape, dtype=kv_dtype, device=k.device)
+    if dv is None:
+        dv = torch.zeros(v.shape, dtype=kv_dtype, device=v.device)
+    _need(dk, "dk", kv_dtype)
+    _need(dv, "dv", kv_dtype)
+    if workspace is None:
+        workspace = alloc_workspace(BS_OP_PACKED_CHUNK_BWD, dims, q.device, nseq, max_seqlen)
+    _check(load_library().bs_attn_packed_chunk_bwd(
+        ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(out_merged), _ptr(lse_merged),
+        _ptr(dout), _ptr(cu_seqlens_q), _ptr(cu_seqlens_k), _ptr(q_pos), _ptr(k_pos), nseq,
+        int(max_seqlen), int(bool(causal)), _scale(scale, q.shape[2]), _ptr(dq_accum), _ptr(dk),
+        _ptr(dv), int(bool(kv_accumulate)), _ptr(workspace), workspace.numel(), _stream(q.device)))
+    return dq_accum, dk, dv
+
+
 def bs_dq_finalize(dq_accum, dq):
     """Rounds the float32 accumulator into dq (bf16 RNE or float32 copy)."""
     _need(dq_accum, "dq_accum", torch.float32, 3)
@@ -284,7 +357,8 @@ def bs_read_device_status(workspace) -> int:
 
 
 def bs_attn_plan_export(op: int, dims: bs_dims, cu_seqlens_q=None, cu_seqlens_k=None, max_seqlen=0,
-                        q_pos_offset=0, k_pos_offset=0, causal=True, device="cuda"):
+                        q_pos_offset=0, k_pos_offset=0, causal=True, device="cuda", q_pos=None,
+                        k_pos=None):
     """Runs the device planner of `op` and returns (items [n,12] int32 numpy, tile_m, tile_n)."""
     import numpy as np
     nseq = cu_seqlens_q.numel() - 1 if cu_seqlens_q is not None else 1
@@ -294,7 +368,8 @@ def bs_attn_plan_export(op: int, dims: bs_dims, cu_seqlens_q=None, cu_seqlens_k=
     count, tm, tn = _SZ(0), _I32(0), _I32(0)
     _check(load_library().bs_attn_plan_export(
         op, ctypes.byref(dims), _ptr(cu_seqlens_q), _ptr(cu_seqlens_k), nseq, int(max_seqlen),
-        int(q_pos_offset), int(k_pos_offset), int(bool(causal)), _ptr(ws), ws.numel(),
+        int(q_pos_offset), int(k_pos_offset), _ptr(q_pos), _ptr(k_pos), int(bool(causal)),
+        _ptr(ws), ws.numel(),
         host.ctypes.data, cap, ctypes.byref(count), ctypes.byref(tm), ctypes.byref(tn),
         _stream(ws.device)))
     return host[:count.value].copy(), tm.value, tn.value

@@ -91,8 +91,19 @@ struct PlanCfg {
   int tile_a, tile_b;
 };
 
-bool is_bwd(int op) { return op == BS_OP_VARLEN_BWD || op == BS_OP_CHUNK_BWD; }
-bool is_varlen(int op) { return op == BS_OP_VARLEN_FWD || op == BS_OP_VARLEN_BWD; }
+bool is_bwd(int op) {
+  return op == BS_OP_VARLEN_BWD || op == BS_OP_CHUNK_BWD || op == BS_OP_PACKED_CHUNK_BWD;
+}
+// ops whose problem is a list of segments (cu_seqlens)
+bool is_varlen(int op) {
+  return op == BS_OP_VARLEN_FWD || op == BS_OP_VARLEN_BWD || op == BS_OP_PACKED_CHUNK_FWD ||
+         op == BS_OP_PACKED_CHUNK_BWD;
+}
+// segment ops whose diagonals come from per-segment global positions
+bool is_packed(int op) { return op == BS_OP_PACKED_CHUNK_FWD || op == BS_OP_PACKED_CHUNK_BWD; }
+// the backward that writes dQ itself (the others add into the caller's fp32 dq_accum)
+bool writes_dq(int op) { return op == BS_OP_VARLEN_BWD; }
+bool valid_op(int op) { return op >= BS_OP_VARLEN_FWD && op <= BS_OP_PACKED_CHUNK_BWD; }
 
 // Plans an op runs, in launch order: the forward walks query tiles; the
 // backward plans twice, query tiles for its dQ kernel, then key tiles for its
@@ -165,7 +176,7 @@ WsLayout layout_of(int op, const bs_dims& d, int64_t nseg) {
   if (is_bwd(op)) {
     L.dvec = off;
     off += align256(sizeof(float) * (size_t)(d.hq * d.total_q));
-    if (varlen && d.dtype == BS_F32) {  // the float32 dQ kernel accumulates
+    if (writes_dq(op) && d.dtype == BS_F32) {  // the float32 dQ kernel accumulates
       L.dq_acc = off;
       off += align256(sizeof(float) * (size_t)(d.total_q * d.hq * d.head_dim));
     }
@@ -187,8 +198,9 @@ int check_ws(const WsLayout& L, const void* ws, size_t bytes) {
 
 // Runs plan `i` of the op; returns the layout with max_items set for that plan.
 hipError_t run_plan(int op, const bs_dims& d, int i, const int32_t* cu_q, const int32_t* cu_k,
-                    int32_t num_seqs, int32_t max_seqlen, int64_t q_off, int64_t k_off,
-                    int causal, void* ws, const WsLayout& L, WsLayout* Lp, hipStream_t s) {
+                    const int64_t* q_pos, const int64_t* k_pos, int32_t num_seqs,
+                    int32_t max_seqlen, int64_t q_off, int64_t k_off, int causal, void* ws,
+                    const WsLayout& L, WsLayout* Lp, hipStream_t s) {
   PlanCfg cfg[2];
   plans_of(op, d.dtype, cfg);
   const bool varlen = is_varlen(op);
@@ -196,15 +208,20 @@ hipError_t run_plan(int op, const bs_dims& d, int i, const int32_t* cu_q, const 
   Lp->max_items = max_items_of(cfg[i], d, varlen ? num_seqs : 1, varlen);
   int64_t diag = q_off - k_off;
   diag = diag < -kDiagClamp ? -kDiagClamp : (diag > kDiagClamp ? kDiagClamp : diag);
+  const bool packed = is_packed(op);
   return launch_plan(cfg[i].kind, varlen ? cu_q : nullptr, varlen ? cu_k : nullptr,
+                     packed ? q_pos : nullptr, packed ? k_pos : nullptr,
                      varlen ? num_seqs : 1, d.total_q, d.total_k, max_seqlen, (int32_t)diag,
                      causal, cfg[i].tile_a, cfg[i].tile_b, Lp->max_items, ws, *Lp, s);
 }
 
-int check_varlen_args(const int32_t* cu_q, const int32_t* cu_k, int32_t num_seqs, int32_t max_seqlen) {
+int check_varlen_args(int op, const int32_t* cu_q, const int32_t* cu_k, const int64_t* q_pos,
+                      const int64_t* k_pos, int32_t num_seqs, int32_t max_seqlen) {
   if (num_seqs < 0) return fail(BS_ERR_INVALID_ARG, "num_seqs = %d < 0", num_seqs);
   if (max_seqlen < 0) return fail(BS_ERR_INVALID_ARG, "max_seqlen = %d < 0", max_seqlen);
   if (cu_q == nullptr || cu_k == nullptr) return fail(BS_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  if (is_packed(op) && num_seqs > 0 && (q_pos == nullptr || k_pos == nullptr))
+    return fail(BS_ERR_INVALID_ARG, "q_pos / k_pos is NULL");
   return BS_OK;
 }
 
@@ -220,9 +237,10 @@ int check_varlen_args(const int32_t* cu_q, const int32_t* cu_k, int32_t num_seqs
   } while (0)
 
 int fwd_common(int op, const bs_dims* dims, const void* q, const void* k, const void* v,
-               const int32_t* cu_q, const int32_t* cu_k, int32_t num_seqs, int32_t max_seqlen,
-               int64_t q_off, int64_t k_off, int causal, float scale, void* out, float* lse,
-               void* ws, size_t ws_bytes, void* stream) {
+               const int32_t* cu_q, const int32_t* cu_k, const int64_t* q_pos,
+               const int64_t* k_pos, int32_t num_seqs, int32_t max_seqlen, int64_t q_off,
+               int64_t k_off, int causal, float scale, void* out, float* lse, void* ws,
+               size_t ws_bytes, void* stream) {
   BS_TRY(check_dims(dims, true));
   const bs_dims& d = *dims;
   const int64_t qn = d.total_q * d.hq * d.head_dim, kn = d.total_k * d.hkv * d.head_dim;
@@ -232,14 +250,15 @@ int fwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
   BS_TRY(check_ptr(out, qn, "out"));
   BS_TRY(check_ptr(lse, d.total_q * d.hq, "lse"));
   BS_TRY(check_scale(scale));
-  if (is_varlen(op)) BS_TRY(check_varlen_args(cu_q, cu_k, num_seqs, max_seqlen));
+  if (is_varlen(op)) BS_TRY(check_varlen_args(op, cu_q, cu_k, q_pos, k_pos, num_seqs, max_seqlen));
   const WsLayout L = layout_of(op, d, is_varlen(op) ? num_seqs : 1);
   BS_TRY(check_ws(L, ws, ws_bytes));
   hipStream_t s = static_cast<hipStream_t>(stream);
   WsLayout Lp;
   {
     ProfScope ps(BS_KERNEL_PLAN, s);
-    BS_HIP(run_plan(op, d, 0, cu_q, cu_k, num_seqs, max_seqlen, q_off, k_off, causal, ws, L, &Lp, s),
+    BS_HIP(run_plan(op, d, 0, cu_q, cu_k, q_pos, k_pos, num_seqs, max_seqlen, q_off, k_off,
+                    causal, ws, L, &Lp, s),
            "planner launch");
   }
   ProfScope ps(BS_KERNEL_FWD, s);
@@ -252,9 +271,10 @@ int fwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
 
 int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const void* v,
                const void* out, const float* lse, const void* dout, const int32_t* cu_q,
-               const int32_t* cu_k, int32_t num_seqs, int32_t max_seqlen, int64_t q_off,
-               int64_t k_off, int causal, float scale, float* dq_accum, void* dq, void* dk,
-               void* dv, int kv_accumulate, void* ws, size_t ws_bytes, void* stream) {
+               const int32_t* cu_k, const int64_t* q_pos, const int64_t* k_pos,
+               int32_t num_seqs, int32_t max_seqlen, int64_t q_off, int64_t k_off, int causal,
+               float scale, float* dq_accum, void* dq, void* dk, void* dv, int kv_accumulate,
+               void* ws, size_t ws_bytes, void* stream) {
   BS_TRY(check_dims(dims, true));
   const bs_dims& d = *dims;
   const int64_t qn = d.total_q * d.hq * d.head_dim, kn = d.total_k * d.hkv * d.head_dim;
@@ -266,27 +286,28 @@ int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
   BS_TRY(check_ptr(dout, qn, "dout"));
   BS_TRY(check_ptr(dk, kn, "dk"));
   BS_TRY(check_ptr(dv, kn, "dv"));
-  const bool varlen = is_varlen(op);
-  if (varlen) BS_TRY(check_ptr(dq, qn, "dq"));
+  const bool varlen = is_varlen(op), direct = writes_dq(op);
+  if (direct) BS_TRY(check_ptr(dq, qn, "dq"));
   else BS_TRY(check_ptr(dq_accum, qn, "dq_accum"));
   BS_TRY(check_scale(scale));
-  if (varlen) BS_TRY(check_varlen_args(cu_q, cu_k, num_seqs, max_seqlen));
+  if (varlen) BS_TRY(check_varlen_args(op, cu_q, cu_k, q_pos, k_pos, num_seqs, max_seqlen));
   const WsLayout L = layout_of(op, d, varlen ? num_seqs : 1);
   BS_TRY(check_ws(L, ws, ws_bytes));
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* base = static_cast<char*>(ws);
   float* dvec = reinterpret_cast<float*>(base + L.dvec);
   const bool f32 = d.dtype == BS_F32;
-  float* acc = varlen ? (f32 ? reinterpret_cast<float*>(base + L.dq_acc) : nullptr) : dq_accum;
+  float* acc = direct ? (f32 ? reinterpret_cast<float*>(base + L.dq_acc) : nullptr) : dq_accum;
   WsLayout Lp;
   {
     ProfScope ps(BS_KERNEL_PLAN, s);
-    BS_HIP(run_plan(op, d, 0, cu_q, cu_k, num_seqs, max_seqlen, q_off, k_off, causal, ws, L, &Lp, s),
+    BS_HIP(run_plan(op, d, 0, cu_q, cu_k, q_pos, k_pos, num_seqs, max_seqlen, q_off, k_off,
+                    causal, ws, L, &Lp, s),
            "planner launch");
   }
   {
     ProfScope ps(BS_KERNEL_PREPROCESS, s);
-    BS_HIP(launch_bwd_preprocess(d, out, dout, dvec, (varlen && f32) ? acc : nullptr, ws, s),
+    BS_HIP(launch_bwd_preprocess(d, out, dout, dvec, (direct && f32) ? acc : nullptr, ws, s),
            "preprocess launch");
   }
   {
@@ -295,13 +316,14 @@ int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
       BS_HIP(launch_bwd_f32_dq(d, q, k, v, lse, dout, dvec, causal, scale, acc, ws, Lp, s),
              "backward dQ launch");
     else
-      BS_HIP(launch_dq_bf16(d, q, k, v, dout, lse, dvec, causal, scale, varlen ? dq : nullptr,
+      BS_HIP(launch_dq_bf16(d, q, k, v, dout, lse, dvec, causal, scale, direct ? dq : nullptr,
                             acc, ws, Lp, s),
              "backward dQ launch");
   }
   {
     ProfScope ps(BS_KERNEL_PLAN, s);
-    BS_HIP(run_plan(op, d, 1, cu_q, cu_k, num_seqs, max_seqlen, q_off, k_off, causal, ws, L, &Lp, s),
+    BS_HIP(run_plan(op, d, 1, cu_q, cu_k, q_pos, k_pos, num_seqs, max_seqlen, q_off, k_off,
+                    causal, ws, L, &Lp, s),
            "planner launch");
   }
   {
@@ -315,7 +337,7 @@ int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
                               ws, Lp, s),
              "backward dK/dV launch");
   }
-  if (varlen && f32) {
+  if (direct && f32) {
     ProfScope ps(BS_KERNEL_FINALIZE, s);
     BS_HIP(launch_dq_finalize(d, acc, dq, ws, s), "dQ finalize launch");
   }
@@ -330,7 +352,7 @@ using namespace bs;
 extern "C" {
 
 size_t bs_attn_workspace_size(int op, const bs_dims* dims, int32_t num_seqs, int32_t max_seqlen) {
-  if (op < BS_OP_VARLEN_FWD || op > BS_OP_CHUNK_BWD) {
+  if (!valid_op(op)) {
     fail(BS_ERR_UNSUPPORTED, "unknown op %d", op);
     return 0;
   }
@@ -347,8 +369,9 @@ int bs_attn_varlen_fwd(const bs_dims* dims, const void* q, const void* k, const 
                        const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k, int32_t num_seqs,
                        int32_t max_seqlen, int causal, float scale, void* out, float* lse,
                        void* workspace, size_t workspace_bytes, void* stream) {
-  return fwd_common(BS_OP_VARLEN_FWD, dims, q, k, v, cu_seqlens_q, cu_seqlens_k, num_seqs,
-                    max_seqlen, 0, 0, causal, scale, out, lse, workspace, workspace_bytes, stream);
+  return fwd_common(BS_OP_VARLEN_FWD, dims, q, k, v, cu_seqlens_q, cu_seqlens_k, nullptr, nullptr,
+                    num_seqs, max_seqlen, 0, 0, causal, scale, out, lse, workspace,
+                    workspace_bytes, stream);
 }
 
 int bs_attn_varlen_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,
@@ -357,16 +380,17 @@ int bs_attn_varlen_bwd(const bs_dims* dims, const void* q, const void* k, const 
                        int32_t max_seqlen, int causal, float scale, void* dq, void* dk, void* dv,
                        void* workspace, size_t workspace_bytes, void* stream) {
   return bwd_common(BS_OP_VARLEN_BWD, dims, q, k, v, out, lse, dout, cu_seqlens_q, cu_seqlens_k,
-                    num_seqs, max_seqlen, 0, 0, causal, scale, nullptr, dq, dk, dv, 0, workspace,
-                    workspace_bytes, stream);
+                    nullptr, nullptr, num_seqs, max_seqlen, 0, 0, causal, scale, nullptr, dq, dk,
+                    dv, 0, workspace, workspace_bytes, stream);
 }
 
 int bs_attn_chunk_fwd(const bs_dims* dims, const void* q, const void* k, const void* v,
                       int64_t q_pos_offset, int64_t k_pos_offset, int causal, float scale,
                       void* out, float* lse, void* workspace, size_t workspace_bytes,
                       void* stream) {
-  return fwd_common(BS_OP_CHUNK_FWD, dims, q, k, v, nullptr, nullptr, 1, 0, q_pos_offset,
-                    k_pos_offset, causal, scale, out, lse, workspace, workspace_bytes, stream);
+  return fwd_common(BS_OP_CHUNK_FWD, dims, q, k, v, nullptr, nullptr, nullptr, nullptr, 1, 0,
+                    q_pos_offset, k_pos_offset, causal, scale, out, lse, workspace,
+                    workspace_bytes, stream);
 }
 
 int bs_attn_chunk_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,
@@ -375,8 +399,31 @@ int bs_attn_chunk_bwd(const bs_dims* dims, const void* q, const void* k, const v
                       float* dq_accum, void* dk, void* dv, int kv_accumulate, void* workspace,
                       size_t workspace_bytes, void* stream) {
   return bwd_common(BS_OP_CHUNK_BWD, dims, q, k, v, out_merged, lse_merged, dout, nullptr, nullptr,
-                    1, 0, q_pos_offset, k_pos_offset, causal, scale, dq_accum, nullptr, dk, dv,
-                    kv_accumulate != 0, workspace, workspace_bytes, stream);
+                    nullptr, nullptr, 1, 0, q_pos_offset, k_pos_offset, causal, scale, dq_accum,
+                    nullptr, dk, dv, kv_accumulate != 0, workspace, workspace_bytes, stream);
+}
+
+int bs_attn_packed_chunk_fwd(const bs_dims* dims, const void* q, const void* k, const void* v,
+                             const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                             const int64_t* q_pos, const int64_t* k_pos, int32_t num_seqs,
+                             int32_t max_seqlen, int causal, float scale, void* out, float* lse,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  return fwd_common(BS_OP_PACKED_CHUNK_FWD, dims, q, k, v, cu_seqlens_q, cu_seqlens_k, q_pos,
+                    k_pos, num_seqs, max_seqlen, 0, 0, causal, scale, out, lse, workspace,
+                    workspace_bytes, stream);
+}
+
+int bs_attn_packed_chunk_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,
+                             const void* out_merged, const float* lse_merged, const void* dout,
+                             const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                             const int64_t* q_pos, const int64_t* k_pos, int32_t num_seqs,
+                             int32_t max_seqlen, int causal, float scale, float* dq_accum,
+                             void* dk, void* dv, int kv_accumulate, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  return bwd_common(BS_OP_PACKED_CHUNK_BWD, dims, q, k, v, out_merged, lse_merged, dout,
+                    cu_seqlens_q, cu_seqlens_k, q_pos, k_pos, num_seqs, max_seqlen, 0, 0, causal,
+                    scale, dq_accum, nullptr, dk, dv, kv_accumulate != 0, workspace,
+                    workspace_bytes, stream);
 }
 
 int bs_dq_finalize(const bs_dims* dims, const float* dq_accum, void* dq, void* stream) {
@@ -419,15 +466,17 @@ int bs_read_device_status(const void* workspace, void* stream) {
 
 int bs_attn_plan_export(int op, const bs_dims* dims, const int32_t* cu_seqlens_q,
                         const int32_t* cu_seqlens_k, int32_t num_seqs, int32_t max_seqlen,
-                        int64_t q_pos_offset, int64_t k_pos_offset, int causal, void* workspace,
+                        int64_t q_pos_offset, int64_t k_pos_offset, const int64_t* q_pos,
+                        const int64_t* k_pos, int causal, void* workspace,
                         size_t workspace_bytes, int32_t* host_items, size_t capacity,
                         size_t* count, int32_t* tile_m, int32_t* tile_n, void* stream) {
-  if (op < BS_OP_VARLEN_FWD || op > BS_OP_CHUNK_BWD) return fail(BS_ERR_UNSUPPORTED, "unknown op %d", op);
+  if (!valid_op(op)) return fail(BS_ERR_UNSUPPORTED, "unknown op %d", op);
   BS_TRY(check_dims(dims, true));
   if (count == nullptr || (capacity > 0 && host_items == nullptr))
     return fail(BS_ERR_INVALID_ARG, "count / host_items is NULL");
   const bool varlen = is_varlen(op);
-  if (varlen) BS_TRY(check_varlen_args(cu_seqlens_q, cu_seqlens_k, num_seqs, max_seqlen));
+  if (varlen)
+    BS_TRY(check_varlen_args(op, cu_seqlens_q, cu_seqlens_k, q_pos, k_pos, num_seqs, max_seqlen));
   const WsLayout L = layout_of(op, *dims, varlen ? num_seqs : 1);
   BS_TRY(check_ws(L, workspace, workspace_bytes));
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -435,8 +484,8 @@ int bs_attn_plan_export(int op, const bs_dims* dims, const int32_t* cu_seqlens_q
   PlanCfg cfg[2];
   const int np = plans_of(op, dims->dtype, cfg);
   WsLayout Lp;
-  BS_HIP(run_plan(op, *dims, np - 1, cu_seqlens_q, cu_seqlens_k, num_seqs, max_seqlen,
-                  q_pos_offset, k_pos_offset, causal, workspace, L, &Lp, s),
+  BS_HIP(run_plan(op, *dims, np - 1, cu_seqlens_q, cu_seqlens_k, q_pos, k_pos, num_seqs,
+                  max_seqlen, q_pos_offset, k_pos_offset, causal, workspace, L, &Lp, s),
          "planner launch");
   WsHeader h;
   BS_HIP(hipMemcpyAsync(&h, workspace, sizeof(h), hipMemcpyDeviceToHost, s), "plan copy");

@@ -210,7 +210,10 @@ __device__ __forceinline__ int swz_tr_off(int k0, int m0, int r, int lane) {
 
 // Host-side launchers implemented in the .hip files (all enqueue on `stream`).
 namespace bs {
-hipError_t launch_plan(PlanKind kind, const int32_t* cu_q, const int32_t* cu_k, int32_t num_seqs,
+// Segments: cu_q/cu_k (NULL: one chunk with diagonal diag_chunk); q_pos/k_pos
+// (NULL: diagonal len_k - len_q of each segment, else q_pos[b] - k_pos[b]).
+hipError_t launch_plan(PlanKind kind, const int32_t* cu_q, const int32_t* cu_k,
+                       const int64_t* q_pos, const int64_t* k_pos, int32_t num_seqs,
                        int64_t total_q, int64_t total_k, int32_t max_seqlen, int32_t diag_chunk,
                        int causal, int tile_a, int tile_b, int64_t max_items, void* ws,
                        const WsLayout& L, hipStream_t stream);

@@ -42,7 +42,11 @@ __device__ __forceinline__ int32_t clamp_diag(int64_t d) {
   return (int32_t)(d < -kDiagClamp ? -kDiagClamp : (d > kDiagClamp ? kDiagClamp : d));
 }
 
-__device__ __forceinline__ Seg load_seg(const int32_t* cu_q, const int32_t* cu_k, int32_t b,
+// Diagonal: key j visible to query i iff j - i <= diag.  Varlen segments are
+// aligned bottom-right (diag = len_k - len_q); packed chunk segments and single
+// chunks take it from the global positions of their first query and key.
+__device__ __forceinline__ Seg load_seg(const int32_t* cu_q, const int32_t* cu_k,
+                                        const int64_t* q_pos, const int64_t* k_pos, int32_t b,
                                         int64_t total_q, int64_t total_k, int32_t diag_chunk) {
   Seg s;
   if (cu_q == nullptr) {  // chunk mode: one segment, diagonal from the offsets
@@ -50,7 +54,7 @@ __device__ __forceinline__ Seg load_seg(const int32_t* cu_q, const int32_t* cu_k
   } else {
     s.q0 = cu_q[b]; s.lq = (int64_t)cu_q[b + 1] - cu_q[b];
     s.k0 = cu_k[b]; s.lk = (int64_t)cu_k[b + 1] - cu_k[b];
-    s.diag = clamp_diag(s.lk - s.lq);
+    s.diag = q_pos == nullptr ? clamp_diag(s.lk - s.lq) : clamp_diag(q_pos[b] - k_pos[b]);
   }
   return s;
 }
@@ -75,7 +79,7 @@ __global__ __launch_bounds__(kCountThreads) void plan_count(
     const int32_t b = base + t;
     int32_t cnt = 0;
     if (b < nseg) {
-      Seg s = load_seg(cu_q, cu_k, b, total_q, total_k, 0);
+      Seg s = load_seg(cu_q, cu_k, nullptr, nullptr, b, total_q, total_k, 0);
       if (s.lq < 0 || s.lk < 0) set_status(&status, BS_DEV_NOT_MONOTONE);
       else if (cu_q != nullptr && (s.lq > max_seqlen || s.lk > max_seqlen)) set_status(&status, BS_DEV_TOO_LONG);
       else {
@@ -104,7 +108,8 @@ __global__ __launch_bounds__(kCountThreads) void plan_count(
 }
 
 __global__ __launch_bounds__(256) void plan_emit(
-    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int32_t num_seqs,
+    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k,
+    const int64_t* __restrict__ q_pos, const int64_t* __restrict__ k_pos, int32_t num_seqs,
     int64_t total_q, int64_t total_k, int32_t diag_chunk, int causal, int kind, int tile_a,
     int tile_b, int64_t max_items, const WsHeader* __restrict__ hdr,
     const int32_t* __restrict__ seg_off, const int32_t* __restrict__ seg_dst,
@@ -119,7 +124,7 @@ __global__ __launch_bounds__(256) void plan_emit(
     if (seg_off[mid] <= i) lo = mid; else hi = mid - 1;
   }
   const int32_t b = lo;
-  const Seg s = load_seg(cu_q, cu_k, b, total_q, total_k, diag_chunk);
+  const Seg s = load_seg(cu_q, cu_k, q_pos, k_pos, b, total_q, total_k, diag_chunk);
   const int64_t tile = i - seg_off[b];
   const int64_t diag = s.diag;
   WorkItem w;
@@ -219,7 +224,8 @@ __global__ __launch_bounds__(256) void plan_rank(const int32_t* __restrict__ cu_
 
 }  // namespace
 
-hipError_t launch_plan(PlanKind kind, const int32_t* cu_q, const int32_t* cu_k, int32_t num_seqs,
+hipError_t launch_plan(PlanKind kind, const int32_t* cu_q, const int32_t* cu_k,
+                       const int64_t* q_pos, const int64_t* k_pos, int32_t num_seqs,
                        int64_t total_q, int64_t total_k, int32_t max_seqlen, int32_t diag_chunk,
                        int causal, int tile_a, int tile_b, int64_t max_items, void* ws,
                        const WsLayout& L, hipStream_t stream) {
@@ -235,8 +241,8 @@ hipError_t launch_plan(PlanKind kind, const int32_t* cu_q, const int32_t* cu_k, 
     hipLaunchKernelGGL(plan_rank, dim3((unsigned)((nseg + 255) / 256)), dim3(256), 0, stream, cu_q,
                        cu_k, num_seqs, hdr, seg_off, seg_dst);
     const unsigned blocks = (unsigned)((max_items + 255) / 256);
-    hipLaunchKernelGGL(plan_emit, dim3(blocks), dim3(256), 0, stream, cu_q, cu_k, num_seqs,
-                       total_q, total_k, diag_chunk, causal, (int)kind, tile_a, tile_b,
+    hipLaunchKernelGGL(plan_emit, dim3(blocks), dim3(256), 0, stream, cu_q, cu_k, q_pos, k_pos,
+                       num_seqs, total_q, total_k, diag_chunk, causal, (int)kind, tile_a, tile_b,
                        max_items, hdr, seg_off, seg_dst, sorted);
   }
   return hipGetLastError();

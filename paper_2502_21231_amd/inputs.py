@@ -1,9 +1,10 @@
 """Seeded synthetic inputs shared by the tests, the benchmark and the oracle checks.
 
-This module only draws numbers: sequence-length mixes shaped after the paper's
-long-tailed datasets (Sec. 3.1, Observation 1, and the skew it reports) and
-i.i.d. N(0,1) tensors.  It holds none of the attention arithmetic, and it
-imports neither the HIP binding nor the oracle.
+This module only draws numbers and lays out indices: sequence-length mixes
+shaped after the paper's long-tailed datasets (Sec. 3.1, Observation 1, and the
+skew it reports), i.i.d. N(0,1) tensors, and the token bookkeeping of the
+zig-zag packing layout (Sec. 7).  It holds none of the attention arithmetic, and
+it imports neither the HIP binding nor the oracle.
 
 Tensors are drawn as float32 from ``numpy.random.default_rng([seed, tensor_id,
 chunk])`` over fixed 4 Mi-element chunks (so the values never depend on the
@@ -101,3 +102,57 @@ def mixed_long_short_lengths(seed: int, total: int = 131072) -> list[int]:
         filled += l
     perm = rng.permutation(len(segs))
     return [segs[i] for i in perm]
+
+
+# ---------------------------------------------------------------- zig-zag packing layout
+# Index bookkeeping only (which tokens a device holds, and the segment tables of one
+# packed call); no attention arithmetic.
+
+def zigzag_parts(lengths, n_dev: int, dev: int):
+    """Parts that device `dev` holds under the symmetric 2N-way split (Sec. 7, Dist-attn
+    with packing): each subsequence (its length a multiple of 2 * n_dev) is cut into 2 * n_dev
+    equal parts and the device holds parts dev and 2 * n_dev - 1 - dev.  Returns, in the
+    device's buffer order (per subsequence: the low part, then the high part), tuples
+    (subsequence, part, global position of the part's first token, part length)."""
+    out = []
+    for s, L in enumerate(lengths):
+        c = L // (2 * n_dev)
+        assert c * 2 * n_dev == L, "subsequence length must be a multiple of 2 * n_dev"
+        for part in (dev, 2 * n_dev - 1 - dev):
+            out.append((s, part, part * c, c))
+    return out
+
+
+def zigzag_step(lengths, n_dev: int, q_dev: int, kv_dev: int, crossed: bool):
+    """Segment table of one packed call in which device q_dev attends to the KV parts that
+    device kv_dev holds: the "straight" call pairs each subsequence's low query part with
+    the low key part and high with high, the "crossed" call low with high and high with low.
+
+    Returns (cu_q, cu_k, q_pos, k_pos, kv_rows): int32 prefix sums over the query buffer of
+    q_dev and over the call's key buffer, int64 global positions of each segment's first
+    query and key, and kv_rows, the rows of kv_dev's buffer (in zigzag_parts order) that make
+    up the call's key buffer, in order (the crossed call swaps each subsequence's two parts)."""
+    qp = zigzag_parts(lengths, n_dev, q_dev)
+    kp = zigzag_parts(lengths, n_dev, kv_dev)
+    kstart = np.concatenate([[0], np.cumsum([p[3] for p in kp])]).astype(np.int64)
+    qlen, klen, qpos, kpos, rows = [], [], [], [], []
+    for i in range(0, len(qp), 2):  # the two parts of one subsequence
+        pairs = [(i, i), (i + 1, i + 1)] if not crossed else [(i, i + 1), (i + 1, i)]
+        for a, b in pairs:
+            qlen.append(qp[a][3])
+            klen.append(kp[b][3])
+            qpos.append(qp[a][2])
+            kpos.append(kp[b][2])
+            rows.append(np.arange(kstart[b], kstart[b] + kp[b][3]))
+    cu_q = np.concatenate([[0], np.cumsum(qlen)]).astype(np.int32)
+    cu_k = np.concatenate([[0], np.cumsum(klen)]).astype(np.int32)
+    return (cu_q, cu_k, np.asarray(qpos, np.int64), np.asarray(kpos, np.int64),
+            np.concatenate(rows) if rows else np.zeros(0, np.int64))
+
+
+def zigzag_rows(lengths, n_dev: int, dev: int):
+    """Row of each token of device `dev`'s buffer in the packed buffer of whole subsequences
+    (subsequences concatenated in order)."""
+    starts = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    return np.concatenate([starts[s] + pos + np.arange(c)
+                           for s, _, pos, c in zigzag_parts(lengths, n_dev, dev)])

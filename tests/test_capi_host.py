@@ -27,7 +27,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 12, names
+    assert len(names) == 14, names
     assert set(names) == set(B.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
@@ -65,6 +65,14 @@ def test_rejects_bad_arguments_without_device(lib):
     assert "smaller" in B.bs_last_error()
     d = dims()
     assert lib.bs_lse_merge(ctypes.byref(d), FAKE, FAKE, 0, FAKE, FAKE, None) == B.BS_ERR_INVALID_ARG
+    # the packed chunk ops need the per-segment positions as well as cu_seqlens
+    assert lib.bs_attn_packed_chunk_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1,
+                                        128, 1, 0.1, FAKE, FAKE, FAKE, 1 << 30, None) == B.BS_ERR_INVALID_ARG
+    assert "q_pos" in B.bs_last_error()
+    assert lib.bs_attn_packed_chunk_bwd(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                        FAKE, FAKE, FAKE, 1, 128, 1, 0.1, None, FAKE, FAKE, 0, FAKE,
+                                        1 << 30, None) == B.BS_ERR_INVALID_ARG
+    assert "dq_accum" in B.bs_last_error()
     assert lib.bs_read_device_status(None, None) == B.BS_ERR_WORKSPACE
 
 
@@ -79,3 +87,7 @@ def test_workspace_size_grows_with_problem(lib):
                                    dims(total_q=4096, total_k=4096, dtype=B.BS_F32), 1, 4096)
     assert f32 >= bwd + 4096 * 4 * 128 * 4
     assert lib.bs_attn_workspace_size(9, ctypes.byref(dims()), 1, 1) == 0
+    # the packed chunk backward adds into the caller's dQ accumulator: no dQ buffer of its own
+    pk = B.bs_attn_workspace_size(B.BS_OP_PACKED_CHUNK_BWD,
+                                  dims(total_q=4096, total_k=4096, dtype=B.BS_F32), 1, 4096)
+    assert bwd <= pk < f32

@@ -212,6 +212,46 @@ def test_zigzag_split_gives_equal_mask_area():
     assert (2 * 4 - 1) * c * c + c * (c + 1) == 8_589_967_360
 
 
+@pytest.mark.parametrize("n_dev", [2, 3])
+def test_packed_zigzag_ring_equals_varlen_attention(n_dev):
+    """Sec. 7 (Dist-attn with packing): every device holds parts i and 2N-1-i of several
+    subsequences in one buffer; over the ring it attends to every device's KV parts, two packed
+    calls per step (straight and crossed part pairs).  Merging a device's partials gives varlen
+    attention over the whole subsequences at its rows; the summed packed backward gives the
+    varlen gradients (dK/dV summed over every device and step, scattered back to the tokens)."""
+    lens = [4 * n_dev, 6 * n_dev, 2 * n_dev * 2]
+    hq, hkv, d, sc = 2, 1, 4, 0.7
+    T = sum(lens)
+    q, k, v, do = (rnd((T, h, d), 300 + i) for i, h in enumerate((hq, hkv, hkv, hq)))
+    cu = lens_to_cu(lens)
+    o_ref, l_ref = A.varlen_fwd(q, k, v, cu, cu, True, sc)
+    dq_ref, dk_ref, dv_ref = A.varlen_bwd(q, k, v, o_ref, l_ref, do, cu, cu, True, sc)
+    dk_sum, dv_sum = np.zeros_like(dk_ref), np.zeros_like(dv_ref)
+    for dev in range(n_dev):
+        rows = inputs.zigzag_rows(lens, n_dev, dev)
+        calls = []
+        for kv_dev in range(n_dev):
+            kv_rows = inputs.zigzag_rows(lens, n_dev, kv_dev)
+            for crossed in (False, True):
+                cu_q, cu_k, qp, kp, kr = inputs.zigzag_step(lens, n_dev, dev, kv_dev, crossed)
+                calls.append((cu_q, cu_k, qp, kp, kv_rows[kr]))
+        parts = [A.packed_chunk_fwd(q[rows], k[g], v[g], cq, ck, qp, kp, True, sc)
+                 for cq, ck, qp, kp, g in calls]
+        om, lm = A.lse_merge(np.stack([p[0] for p in parts]), np.stack([p[1] for p in parts]))
+        assert np.allclose(om, o_ref[rows], atol=1e-12)
+        assert np.allclose(lm, l_ref[:, rows], atol=1e-12)
+        dq = np.zeros((len(rows), hq, d))
+        for cq, ck, qp, kp, g in calls:
+            a, b_, c_ = A.packed_chunk_bwd(q[rows], k[g], v[g], om, lm, do[rows], cq, ck, qp, kp,
+                                           True, sc)
+            dq += a
+            np.add.at(dk_sum, g, b_)
+            np.add.at(dv_sum, g, c_)
+        assert np.allclose(dq, dq_ref[rows], atol=1e-12)
+    assert np.allclose(dk_sum, dk_ref, atol=1e-12)
+    assert np.allclose(dv_sum, dv_ref, atol=1e-12)
+
+
 def test_visible_pairs_bruteforce():
     for lq, lk, diag in [(5, 5, 0), (3, 7, 4), (7, 3, -4), (6, 6, 10), (6, 6, -10), (9, 4, 2)]:
         brute = int(A.visible_mask(lq, lk, diag, True).sum())

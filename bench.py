@@ -70,7 +70,13 @@ WORKLOADS = {
             "KV chunks of 32768 (7 past, 1 diagonal), fwd x8 + LSE merge + bwd x8",
     "zigzag141b": "141B-shaped zig-zag CP share: 48 q heads, 8 kv heads, Q halves of 32768 at 0 "
                   "and 229376 against the matching KV halves, fwd + merge + bwd",
+    "zigzag_packed7b": "7B-shaped packed CP share (dist-attn with packing): device 0 of a 4-way "
+                       "zig-zag split of 4 subsequences (131072, 65536, 32768, 32768 tokens), its "
+                       "2 parts of each (65536 query tokens) against every device's KV parts over "
+                       "the ring: 8 packed calls fwd + 8-way merge + 8 packed calls bwd; 32 q "
+                       "heads, 32 kv heads, head_dim 128",
 }
+ZIGZAG_PACKED = dict(lens=[131072, 65536, 32768, 32768], n_dev=4, dev=0, hq=32, hkv=32, d=128)
 
 
 def log(msg):
@@ -313,6 +319,78 @@ def run_chunk_bench(args, dev):
     return res
 
 
+def run_zigzag_packed_bench(args, dev):
+    """The packed context-parallel share of one device over a whole ring: each ring step is two
+    packed calls (straight and crossed part pairs).  The key buffers of both layouts are staged
+    before timing (laying them out is the ring transport's job); every call writes its own dK, dV."""
+    import numpy as np
+    import torch
+    from paper_2502_21231_amd import bs_attn as B
+    from paper_2502_21231_amd import inputs
+    cfg = ZIGZAG_PACKED
+    lens, n_dev, me, hq, hkv, d = (cfg[k] for k in ("lens", "n_dev", "dev", "hq", "hkv", "d"))
+    seed = args.seed
+    scale = 1.0 / math.sqrt(d)
+    T = sum(lens)
+    rows = torch.from_numpy(inputs.zigzag_rows(lens, n_dev, me))
+    q = inputs.normal(seed, inputs.TID_Q, (T, hq, d))[rows].to(dev)
+    do = inputs.normal(seed, inputs.TID_DO, (T, hq, d))[rows].to(dev)
+    k_all = inputs.normal(seed, inputs.TID_K, (T, hkv, d))
+    v_all = inputs.normal(seed, inputs.TID_V, (T, hkv, d))
+    calls, A = [], 0
+    for kv_dev in range(n_dev):
+        kv_rows = inputs.zigzag_rows(lens, n_dev, kv_dev)
+        for crossed in (False, True):
+            cu_q, cu_k, qp, kp, kr = inputs.zigzag_step(lens, n_dev, me, kv_dev, crossed)
+            g = torch.from_numpy(kv_rows[kr])
+            calls.append(dict(k=k_all[g].to(dev), v=v_all[g].to(dev),
+                              cu_q=torch.from_numpy(cu_q).to(dev), cu_k=torch.from_numpy(cu_k).to(dev),
+                              qp=torch.from_numpy(qp).to(dev), kp=torch.from_numpy(kp).to(dev)))
+            for b in range(len(qp)):
+                A += visible_pairs_chunk_closed(int(cu_q[b + 1] - cu_q[b]), int(cu_k[b + 1] - cu_k[b]),
+                                                int(qp[b] - kp[b]))
+    del k_all, v_all
+    maxlen = max(lens)
+    n = len(calls)
+    Tq = q.shape[0]
+    dims = B.make_dims(q, calls[0]["k"])
+    ws_f = B.alloc_workspace(B.BS_OP_PACKED_CHUNK_FWD, dims, dev, len(lens) * 2, maxlen)
+    ws_b = B.alloc_workspace(B.BS_OP_PACKED_CHUNK_BWD, dims, dev, len(lens) * 2, maxlen)
+    parts_o = torch.empty(n, Tq, hq, d, dtype=torch.bfloat16, device=dev)
+    parts_l = torch.empty(n, hq, Tq, dtype=torch.float32, device=dev)
+    O = torch.empty(Tq, hq, d, dtype=torch.bfloat16, device=dev)
+    L = torch.empty(hq, Tq, dtype=torch.float32, device=dev)
+    dq_acc = torch.empty(Tq, hq, d, dtype=torch.float32, device=dev)
+    dQ = torch.empty_like(q)
+    dK = [torch.empty_like(c["k"]) for c in calls]
+    dV = [torch.empty_like(c["v"]) for c in calls]
+
+    def step():
+        for i, c in enumerate(calls):
+            B.bs_attn_packed_chunk_fwd(q, c["k"], c["v"], c["cu_q"], c["cu_k"], c["qp"], c["kp"], maxlen,
+                                       True, scale, parts_o[i], parts_l[i], ws_f)
+        B.bs_lse_merge(parts_o, parts_l, O, L)
+        dq_acc.zero_()
+        for i, c in enumerate(calls):
+            B.bs_attn_packed_chunk_bwd(q, c["k"], c["v"], O, L, do, c["cu_q"], c["cu_k"], c["qp"], c["kp"],
+                                       maxlen, True, scale, dq_acc, dK[i], dV[i], False, ws_b)
+        B.bs_dq_finalize(dq_acc, dQ)
+
+    flops_fwd = 4 * d * hq * A
+    flops_bwd = 10 * d * hq * A
+    res = time_steps(step, args, dev, flops_fwd, flops_bwd)
+    res["config"] = {"workload": WORKLOADS[args.workload], "subsequences": lens, "devices": n_dev,
+                     "device": me, "query_tokens": Tq, "packed_calls_per_pass": n, "heads_q": hq,
+                     "heads_kv": hkv, "head_dim": d, "seed": seed, "visible_pairs": A}
+    res["flops_per_step"] = flops_fwd + flops_bwd
+    res["value_half_s2"] = res["value"] * (A - Tq / 2) / A
+    merge = res["kernels"].get("lse_merge")
+    if merge:
+        nbytes = n * Tq * hq * d * 2 + n * hq * Tq * 4 + Tq * hq * d * 2 + hq * Tq * 4
+        res["lse_merge_gbs"] = nbytes / (merge["avg_ms_per_launch"] * 1e-3) / 1e9
+    return res
+
+
 def visible_pairs_chunk_closed(lq, lk, diag):
     """Exact visible (query, key) pairs of a chunk pair: key j visible to query i iff j - i <= diag."""
     tot = 0
@@ -362,6 +440,8 @@ def main():
     dev = torch.device("cuda:0")
     if args.workload in ("packed7b", "gqa70b"):
         res = run_varlen_bench(args, dev)
+    elif args.workload == "zigzag_packed7b":
+        res = run_zigzag_packed_bench(args, dev)
     else:
         res = run_chunk_bench(args, dev)
     line = {

@@ -199,3 +199,91 @@ def test_zigzag_share_141b_256k(gpu):
     """Device 0 of a 4-way symmetric split: Q/KV parts 0 and 7 of a 256K sequence, 48/8 heads."""
     c = 32768
     chunk_share(48, 8, [0, 7 * c], [0, 7 * c], [(i, j) for i in range(2) for j in range(2)], 0)
+
+
+def test_zigzag_packed_7b_fullsize(gpu):
+    """The packed context-parallel share of the benchmark (device 0 of a 4-way zig-zag split of
+    four subsequences, 8 packed calls each way, 32/32 heads): sampled rows of the merged O, LSE and
+    the summed dQ against attention over the whole subsequence; dK/dV of the last keys of the
+    largest subsequence's first part; and over all calls, per KV head, sum dK = 0 and
+    sum dV = sum of the device's dO rows (every row's P sums to 1 over the ring)."""
+    lens, n_dev, me, hq, hkv, seed = [131072, 65536, 32768, 32768], 4, 0, 32, 32, 0
+    T = sum(lens)
+    rows = inputs.zigzag_rows(lens, n_dev, me)
+    rows_t = torch.from_numpy(rows)
+    q_all = gen(seed, inputs.TID_Q, (T, hq, D))
+    do_all = gen(seed, inputs.TID_DO, (T, hq, D))
+    k_all = gen(seed, inputs.TID_K, (T, hkv, D))
+    v_all = gen(seed, inputs.TID_V, (T, hkv, D))
+    qg, dog = q_all[rows_t].cuda(), do_all[rows_t].cuda()
+    maxlen = max(lens)
+    calls = []
+    for kv_dev in range(n_dev):
+        kv_rows = inputs.zigzag_rows(lens, n_dev, kv_dev)
+        for crossed in (False, True):
+            cu_q, cu_k, qp, kp, kr = inputs.zigzag_step(lens, n_dev, me, kv_dev, crossed)
+            g = torch.from_numpy(kv_rows[kr])
+            calls.append(dict(rows=kv_rows[kr], k=k_all[g].cuda(), v=v_all[g].cuda(),
+                              a=[torch.from_numpy(x).cuda() for x in (cu_q, cu_k, qp, kp)]))
+    parts = [B.bs_attn_packed_chunk_fwd(qg, c["k"], c["v"], *c["a"], maxlen, True, SCALE) for c in calls]
+    om, lm = B.bs_lse_merge(torch.stack([p[0] for p in parts]), torch.stack([p[1] for p in parts]))
+    del parts
+    acc = torch.zeros(len(rows), hq, D, dtype=torch.float32, device="cuda")
+    sk = torch.zeros(hkv, D, dtype=torch.float64, device="cuda")
+    sv = torch.zeros_like(sk)
+    first = None
+    for i, c in enumerate(calls):
+        _, dk, dv = B.bs_attn_packed_chunk_bwd(qg, c["k"], c["v"], om, lm, dog, *c["a"], maxlen, True,
+                                               SCALE, dq_accum=acc)
+        assert torch.isfinite(dk.float()).all() and torch.isfinite(dv.float()).all()
+        sk += dk.double().sum(dim=0)
+        sv += dv.double().sum(dim=0)
+        if i == 0:
+            first = (dk.cpu(), dv.cpu())  # straight call against the device's own parts
+    dq = B.bs_dq_finalize(acc, torch.empty_like(qg))
+    torch.cuda.synchronize()
+    om_c, lm_c, dq_c = om.cpu(), lm.cpu(), dq.cpu()
+    assert torch.isfinite(om_c.float()).all() and torch.isfinite(dq_c.float()).all()
+
+    # sampled query rows: buffer row -> (subsequence, position), against all of its keys
+    starts = np.concatenate([[0], np.cumsum(lens)])
+    parts_of = inputs.zigzag_parts(lens, n_dev, me)
+    rng = np.random.default_rng(7)
+    off = 0
+    for s_idx, part, pos0, c_len in parts_of:
+        picks = sorted({0, c_len - 1, int(rng.integers(0, c_len))})
+        for i in picks:
+            r = off + i                      # row of the device buffer
+            p = pos0 + i                     # position inside the subsequence
+            for h in sorted({0, hq - 1, int(rng.integers(0, hq))}):
+                K = k_all[starts[s_idx]:starts[s_idx + 1], h:h + 1]
+                V = v_all[starts[s_idx]:starts[s_idx + 1], h:h + 1]
+                qrow = q_all[rows[r]:rows[r] + 1, h:h + 1]
+                dorow = do_all[rows[r]:rows[r] + 1, h:h + 1]
+                o, l, gq = row_oracle(qrow, K, V, dorow, p, 0)
+                check_close(f"O s{s_idx} part{part} row{i} h{h}", f64(om_c[r, h]), o[0, 0], 2e-2, True)
+                check_lse(f"LSE s{s_idx} part{part} row{i} h{h}", f64(lm_c[h, r:r + 1]), l[0], 1e-3)
+                check_close(f"dQ s{s_idx} part{part} row{i} h{h}", f64(dq_c[r, h]), gq[0, 0], 2e-2, True)
+        off += c_len
+
+    # dK, dV of the last 48 keys of subsequence 0's part 0 in the straight call with the device's
+    # own parts: only the device's part-0 query rows from there on see them
+    c0 = lens[0] // (2 * n_dev)
+    r0 = c0 - 48
+    dk0, dv0 = first
+    for hk in (0, hkv - 1):
+        qb = q_all[r0:c0, hk:hk + 1]        # subsequence 0 starts at row 0, part 0 at position 0
+        dob = do_all[r0:c0, hk:hk + 1]
+        K, V = k_all[0:c0, hk:hk + 1], v_all[0:c0, hk:hk + 1]
+        o_in = om_c[r0:c0, hk:hk + 1]       # the merged results of those rows (the device's rows 0..)
+        l_in = lm_c[hk:hk + 1, r0:c0]
+        _, gk, gv = A.chunk_bwd(qb, K, V, o_in, l_in, dob, r0, 0, True, SCALE)
+        check_close(f"dK part0 hk{hk}", f64(dk0[r0:c0, hk:hk + 1]), gk[r0:], 2e-2, True)
+        check_close(f"dV part0 hk{hk}", f64(dv0[r0:c0, hk:hk + 1]), gv[r0:], 2e-2, True)
+
+    # over all calls: sum dK = 0, sum dV = sum dO of the device's rows (MHA: per head)
+    so = dog.double().sum(dim=0)
+    n = len(rows)
+    tol = 0.02 * math.sqrt(n) + 1e-3 * float(so.abs().max())
+    assert float(sk.abs().max()) <= tol, ("sum dK", float(sk.abs().max()), tol)
+    assert float((sv - so).abs().max()) <= tol, ("sum dV", float((sv - so).abs().max()), tol)

@@ -68,6 +68,12 @@ WORKLOADS = {
               "head_dim 128, 131072 tokens, 1-2 long segments (32K-64K) + U[256,4K] shorts",
     "cp7b": "context-parallel share on the 7B shape: a 32768-token Q chunk at offset 1015808 vs 8 "
             "KV chunks of 32768 (7 past, 1 diagonal), fwd x8 + LSE merge + bwd x8",
+    "cp7b_ring": "the cp7b share run as one device of an 8-step ring on one GPU: its own (diagonal) "
+                 "KV shard first, then the 7 before it, each next shard received by a device copy "
+                 "on a second HIP stream into a double buffer while the current step computes; "
+                 "every forward step folded into a running float32 (O, LSE) in the kernel epilogue "
+                 "(no partials, no merge pass); the backward receives the shards the same way and "
+                 "sends each shard's dK, dV out on the copy stream",
     "zigzag141b": "141B-shaped zig-zag CP share: 48 q heads, 8 kv heads, Q halves of 32768 at 0 "
                   "and 229376 against the matching KV halves, fwd + merge + bwd",
     "zigzag_packed7b": "7B-shaped packed CP share (dist-attn with packing): device 0 of a 4-way "
@@ -319,6 +325,45 @@ def run_chunk_bench(args, dev):
     return res
 
 
+def run_cp_ring_bench(args, dev):
+    """cp7b through the single-GPU ring rehearsal (paper_2502_21231_amd.ring.ChunkRing): same
+    shards, seeds and FLOPs as cp7b; the timed step also carries every shard transfer."""
+    import torch
+    from paper_2502_21231_amd import inputs
+    from paper_2502_21231_amd.ring import ChunkRing
+    hq, hkv, c, q_offs, kv_offs, pairs = chunk_workload("cp7b")
+    d, seed = 128, args.seed
+    scale = 1.0 / math.sqrt(d)
+    q = inputs.normal(seed, inputs.TID_Q, (c, hq, d)).to(dev)
+    do = inputs.normal(seed, inputs.TID_DO, (c, hq, d)).to(dev)
+    order = sorted(range(len(kv_offs)), key=lambda j: -kv_offs[j])  # own shard, then those behind
+    K = [inputs.normal(seed, inputs.tid_chunk_k(j), (c, hkv, d)).to(dev) for j in order]
+    V = [inputs.normal(seed, inputs.tid_chunk_v(j), (c, hkv, d)).to(dev) for j in order]
+    ring = ChunkRing(q, do, K, V, q_offs[0], [kv_offs[j] for j in order], True, scale,
+                     time_copies=True)
+
+    def step():
+        ring.forward()
+        ring.backward()
+
+    A = sum(visible_pairs_chunk_closed(c, c, q_offs[0] - kv_offs[j]) for j in order)
+    flops_fwd = 4 * d * hq * A
+    flops_bwd = 10 * d * hq * A
+    res = time_steps(step, args, dev, flops_fwd, flops_bwd)
+    copy_ms, copy_bytes = ring.copy_stats()  # every copy of the warmup and timed steps
+    n_steps = args.warmup + args.steps
+    res["config"] = {"workload": WORKLOADS[args.workload], "chunk_tokens": c, "heads_q": hq,
+                     "heads_kv": hkv, "head_dim": d, "q_offsets": q_offs,
+                     "kv_offsets_in_ring_order": [kv_offs[j] for j in order], "seed": seed,
+                     "visible_pairs": A}
+    res["flops_per_step"] = flops_fwd + flops_bwd
+    res["value_half_s2"] = res["value"] * (A - c / 2) / A
+    # transfers per step: 7 shards received in each pass, 8 shards' dK, dV sent
+    res["ring_copies"] = {"ms_per_step": copy_ms / n_steps, "bytes_per_step": copy_bytes / n_steps,
+                          "gbs": copy_bytes / (copy_ms * 1e-3) / 1e9 if copy_ms > 0 else None}
+    return res
+
+
 def run_zigzag_packed_bench(args, dev):
     """The packed context-parallel share of one device over a whole ring: each ring step is two
     packed calls (straight and crossed part pairs).  The key buffers of both layouts are staged
@@ -442,6 +487,8 @@ def main():
         res = run_varlen_bench(args, dev)
     elif args.workload == "zigzag_packed7b":
         res = run_zigzag_packed_bench(args, dev)
+    elif args.workload == "cp7b_ring":
+        res = run_cp_ring_bench(args, dev)
     else:
         res = run_chunk_bench(args, dev)
     line = {
@@ -459,6 +506,7 @@ def main():
         "kernels": res["kernels"], "flops_per_step": res["flops_per_step"],
         "roofline": res["roofline"],
         "lse_merge_gbs": res.get("lse_merge_gbs"),
+        "ring_copies": res.get("ring_copies"),
         "cpu_baseline": res.get("cpu_baseline"),
     }
     print(json.dumps(line), flush=True)

@@ -31,7 +31,8 @@
  *     from a caller-provided workspace sized by bs_attn_workspace_size().
  *   - Layouts (row-major):  Q, O, dO, dQ: [T, hq, head_dim];
  *     K, V, dK, dV: [Tk, hkv, head_dim];  LSE and D: float32 [hq, T];
- *     merge partials: O [n, T, hq, head_dim], LSE [n, hq, T].
+ *     merge partials: O [n, T, hq, head_dim], LSE [n, hq, T]; running merge
+ *     state: o_run float32 [T, hq, head_dim], lse_run float32 [hq, T].
  *   - Element type of Q/K/V/O/dO/dQ/dK/dV is dims->dtype: BS_BF16 (bf16 in,
  *     fp32 accumulation, round-to-nearest-even on every bf16 store) or BS_F32.
  *     LSE is always float32 (natural log).
@@ -136,11 +137,33 @@ int bs_attn_varlen_bwd(const bs_dims* dims, const void* q, const void* k, const 
  * q_pos_offset, against a KV shard of total_k tokens at k_pos_offset.  With
  * causal != 0 key j is visible to query i iff k_pos_offset + j <= q_pos_offset + i.
  * Writes this step's partial out [T, hq, d] and lse [hq, T]; rows that see no
- * key get out = 0, lse = -inf.  Combine the steps with bs_lse_merge(). */
+ * key get out = 0, lse = -inf.  Combine the steps with bs_lse_merge(), or use
+ * bs_attn_chunk_fwd_merge() to combine each step as it is computed. */
 int bs_attn_chunk_fwd(const bs_dims* dims, const void* q, const void* k, const void* v,
                       int64_t q_pos_offset, int64_t k_pos_offset, int causal, float scale,
                       void* out, float* lse, void* workspace, size_t workspace_bytes,
                       void* stream);
+
+/* One context-parallel step folded into a running result as it arrives (the ring
+ * steps of Sec. 2.4 overlap the key exchange with compute, so each step's output
+ * can be combined at once instead of stored and merged at the end).  The mask and
+ * the positions are those of bs_attn_chunk_fwd; workspace as for BS_OP_CHUNK_FWD.
+ * Running state, owned by the caller: o_run float32 [T, hq, d] and lse_run
+ * float32 [hq, T] (natural log).  With accumulate == 0 the running state is
+ * replaced by this step's result (rows that see no key: o 0, lse -inf); with
+ * accumulate != 0 it is combined with it by the rule of bs_lse_merge(),
+ *   LSE' = log(exp(LSE) + exp(LSE_step)),
+ *   O'   = exp(LSE - LSE') O + exp(LSE_step - LSE') O_step,
+ * computed in float32 without rounding O_step to dims->dtype; a row whose running
+ * LSE is -inf ignores its o_run contents.  out: NULL, or [T, hq, d] of
+ * dims->dtype, not overlapping o_run; when given, the combined O is written there
+ * (rounded once) instead of into o_run, which this call then leaves as it was
+ * (pass it on a ring's last step); lse_run is updated either way.  Every query
+ * row is written on every call, including rows that see no key of this step. */
+int bs_attn_chunk_fwd_merge(const bs_dims* dims, const void* q, const void* k, const void* v,
+                            int64_t q_pos_offset, int64_t k_pos_offset, int causal, float scale,
+                            float* o_run, float* lse_run, int accumulate, void* out,
+                            void* workspace, size_t workspace_bytes, void* stream);
 
 /* Backward of one context-parallel step.  out_merged / lse_merged are the
  * final (merged over all steps) forward results.  Adds this step's dQ
@@ -180,6 +203,18 @@ int bs_attn_packed_chunk_fwd(const bs_dims* dims, const void* q, const void* k, 
                              int32_t max_seqlen, int causal, float scale, void* out, float* lse,
                              void* workspace, size_t workspace_bytes, void* stream);
 
+/* Packed context-parallel step folded into a running result: the segments, mask
+ * and positions of bs_attn_packed_chunk_fwd with the running state (o_run, lse_run,
+ * accumulate, out) of bs_attn_chunk_fwd_merge; workspace as for
+ * BS_OP_PACKED_CHUNK_FWD. */
+int bs_attn_packed_chunk_fwd_merge(const bs_dims* dims, const void* q, const void* k,
+                                   const void* v, const int32_t* cu_seqlens_q,
+                                   const int32_t* cu_seqlens_k, const int64_t* q_pos,
+                                   const int64_t* k_pos, int32_t num_seqs, int32_t max_seqlen,
+                                   int causal, float scale, float* o_run, float* lse_run,
+                                   int accumulate, void* out, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
 /* Backward of one packed context-parallel step, with the conventions of
  * bs_attn_chunk_bwd: out_merged / lse_merged are the final forward results of
  * these query rows, this step's dQ is added into dq_accum (float32 [T, hq, d]),
@@ -205,6 +240,16 @@ int bs_dq_finalize(const bs_dims* dims, const float* dq_accum, void* dq, void* s
  * [T, hq, d] and lse [hq, T].  n must be >= 1. */
 int bs_lse_merge(const bs_dims* dims, const void* out_partials, const float* lse_partials,
                  int32_t n, void* out, float* lse, void* stream);
+
+/* Device-to-device copy of `bytes` on `stream` by the GPU's DMA engines, leaving
+ * the compute units to the attention kernels that it overlaps (the copies that
+ * Sec. 5.2, Selective Offloading, overlaps with compute run on DMA engines rather
+ * than on the streaming multiprocessors for the same reason).  It stands in for
+ * the transfer of a KV shard or of its gradients between ring neighbours when
+ * one GPU rehearses a device's ring (Sec. 2.4).  dst and src: device pointers of
+ * at least `bytes` bytes, not overlapping (BS_ERR_INVALID_ARG); bytes == 0
+ * enqueues nothing. */
+int bs_copy_async(void* dst, const void* src, size_t bytes, void* stream);
 
 /* TEST HELPER (synchronises `stream`): the device status word left in the
  * workspace by the last planning kernel; BS_OK, or BS_ERR_DEVICE_STATUS with

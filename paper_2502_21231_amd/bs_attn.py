@@ -25,6 +25,7 @@ BS_F32, BS_BF16 = 0, 1
 EXPORTS = (
     "bs_attn_workspace_size", "bs_attn_varlen_fwd", "bs_attn_varlen_bwd", "bs_attn_chunk_fwd",
     "bs_attn_chunk_bwd", "bs_attn_packed_chunk_fwd", "bs_attn_packed_chunk_bwd",
+    "bs_attn_chunk_fwd_merge", "bs_attn_packed_chunk_fwd_merge", "bs_copy_async",
     "bs_dq_finalize", "bs_lse_merge", "bs_read_device_status",
     "bs_attn_plan_export", "bs_set_profiling", "bs_profile_read", "bs_last_error",
 )
@@ -72,8 +73,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "bs_attn_packed_chunk_bwd": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                                     _I32, _I32, ctypes.c_int, _F, _P, _P, _P,
                                                     ctypes.c_int, _P, _SZ, _P]),
+        "bs_attn_chunk_fwd_merge": (ctypes.c_int, [_DIMS, _P, _P, _P, _I64, _I64, ctypes.c_int, _F,
+                                                   _P, _P, ctypes.c_int, _P, _P, _SZ, _P]),
+        "bs_attn_packed_chunk_fwd_merge": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _P, _I32,
+                                                          _I32, ctypes.c_int, _F, _P, _P,
+                                                          ctypes.c_int, _P, _P, _SZ, _P]),
         "bs_dq_finalize": (ctypes.c_int, [_DIMS, _P, _P, _P]),
         "bs_lse_merge": (ctypes.c_int, [_DIMS, _P, _P, _I32, _P, _P, _P]),
+        "bs_copy_async": (ctypes.c_int, [_P, _P, _SZ, _P]),
         "bs_read_device_status": (ctypes.c_int, [_P, _P]),
         "bs_attn_plan_export": (ctypes.c_int, [ctypes.c_int, _DIMS, _P, _P, _I32, _I32, _I64, _I64,
                                                _P, _P, ctypes.c_int, _P, _SZ, _P, _SZ,
@@ -293,6 +300,56 @@ def bs_attn_packed_chunk_fwd(q, k, v, cu_seqlens_q, cu_seqlens_k, q_pos, k_pos, 
     return out, lse
 
 
+def _running(q, o_run, lse_run, out):
+    _need(o_run, "o_run", torch.float32)
+    _need(lse_run, "lse_run", torch.float32)
+    if o_run.shape != q.shape or lse_run.shape != (q.shape[1], q.shape[0]):
+        raise ValueError("o_run must be [T, hq, d] and lse_run [hq, T] of the queries")
+    if out is not None:
+        _need(out, "out", q.dtype)
+        if out.shape != q.shape:
+            raise ValueError("out must be [T, hq, d]")
+
+
+def bs_attn_chunk_fwd_merge(q, k, v, q_pos_offset: int, k_pos_offset: int, o_run, lse_run,
+                            accumulate: bool, causal: bool = True, scale: float | None = None,
+                            out=None, workspace=None):
+    """One context-parallel step folded into the running (o_run float32 [T,Hq,d],
+    lse_run float32 [Hq,T]): replaced (accumulate False) or combined by log-sum-exp
+    weights.  With `out` the combined output is written there in q's dtype instead of
+    into o_run.  Returns (o_run, lse_run, out)."""
+    _qkv(q, k, v)
+    _running(q, o_run, lse_run, out)
+    dims = make_dims(q, k)
+    if workspace is None:
+        workspace = alloc_workspace(BS_OP_CHUNK_FWD, dims, q.device)
+    _check(load_library().bs_attn_chunk_fwd_merge(
+        ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), int(q_pos_offset), int(k_pos_offset),
+        int(bool(causal)), _scale(scale, q.shape[2]), _ptr(o_run), _ptr(lse_run),
+        int(bool(accumulate)), _ptr(out), _ptr(workspace), workspace.numel(), _stream(q.device)))
+    return o_run, lse_run, out
+
+
+def bs_attn_packed_chunk_fwd_merge(q, k, v, cu_seqlens_q, cu_seqlens_k, q_pos, k_pos,
+                                   max_seqlen: int, o_run, lse_run, accumulate: bool,
+                                   causal: bool = True, scale: float | None = None, out=None,
+                                   workspace=None):
+    """Packed context-parallel step (segments as in bs_attn_packed_chunk_fwd) folded into
+    the running (o_run, lse_run) as in bs_attn_chunk_fwd_merge.  Returns (o_run, lse_run, out)."""
+    _qkv(q, k, v)
+    nseq = _segments(cu_seqlens_q, cu_seqlens_k, q_pos, k_pos)
+    _running(q, o_run, lse_run, out)
+    dims = make_dims(q, k)
+    if workspace is None:
+        workspace = alloc_workspace(BS_OP_PACKED_CHUNK_FWD, dims, q.device, nseq, max_seqlen)
+    _check(load_library().bs_attn_packed_chunk_fwd_merge(
+        ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_q), _ptr(cu_seqlens_k),
+        _ptr(q_pos), _ptr(k_pos), nseq, int(max_seqlen), int(bool(causal)),
+        _scale(scale, q.shape[2]), _ptr(o_run), _ptr(lse_run), int(bool(accumulate)), _ptr(out),
+        _ptr(workspace), workspace.numel(), _stream(q.device)))
+    return o_run, lse_run, out
+
+
 def bs_attn_packed_chunk_bwd(q, k, v, out_merged, lse_merged, dout, cu_seqlens_q, cu_seqlens_k,
                              q_pos, k_pos, max_seqlen: int, causal: bool = True,
                              scale: float | None = None, dq_accum=None, dk=None, dv=None,
@@ -348,6 +405,18 @@ def bs_lse_merge(out_partials, lse_partials, out=None, lse=None):
     _check(load_library().bs_lse_merge(ctypes.byref(dims), _ptr(out_partials), _ptr(lse_partials), n,
                                        _ptr(out), _ptr(lse), _stream(out_partials.device)))
     return out, lse
+
+
+def bs_copy_async(dst, src):
+    """dst.copy_(src) on the current stream by the GPU's DMA engines (same dtype and size,
+    both contiguous on the GPU); returns dst."""
+    _need(dst, "dst")
+    _need(src, "src")
+    if dst.dtype != src.dtype or dst.numel() != src.numel():
+        raise ValueError("dst and src must have the same dtype and number of elements")
+    _check(load_library().bs_copy_async(_ptr(dst), _ptr(src), src.numel() * src.element_size(),
+                                        _stream(src.device)))
+    return dst
 
 
 def bs_read_device_status(workspace) -> int:

@@ -236,19 +236,37 @@ int check_varlen_args(int op, const int32_t* cu_q, const int32_t* cu_k, const in
     if (e__ != hipSuccess) return hip_fail(e__, what); \
   } while (0)
 
+// True when the byte ranges [a, a + na) and [b, b + nb) intersect.
+bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return na > 0 && nb > 0 && x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+// merge == NULL: writes the step's (out, lse).  Otherwise folds the step into the
+// running (merge->o_run, merge->lse_run); out is then optional (the final output).
 int fwd_common(int op, const bs_dims* dims, const void* q, const void* k, const void* v,
                const int32_t* cu_q, const int32_t* cu_k, const int64_t* q_pos,
                const int64_t* k_pos, int32_t num_seqs, int32_t max_seqlen, int64_t q_off,
-               int64_t k_off, int causal, float scale, void* out, float* lse, void* ws,
-               size_t ws_bytes, void* stream) {
+               int64_t k_off, int causal, float scale, void* out, float* lse,
+               const FwdMerge* merge, void* ws, size_t ws_bytes, void* stream) {
   BS_TRY(check_dims(dims, true));
   const bs_dims& d = *dims;
   const int64_t qn = d.total_q * d.hq * d.head_dim, kn = d.total_k * d.hkv * d.head_dim;
   BS_TRY(check_ptr(q, qn, "q"));
   BS_TRY(check_ptr(k, kn, "k"));
   BS_TRY(check_ptr(v, kn, "v"));
-  BS_TRY(check_ptr(out, qn, "out"));
-  BS_TRY(check_ptr(lse, d.total_q * d.hq, "lse"));
+  if (merge == nullptr) {
+    BS_TRY(check_ptr(out, qn, "out"));
+    BS_TRY(check_ptr(lse, d.total_q * d.hq, "lse"));
+  } else {
+    BS_TRY(check_ptr(merge->o_run, qn, "o_run"));
+    BS_TRY(check_ptr(merge->lse_run, d.total_q * d.hq, "lse_run"));
+    if (out != nullptr) {
+      BS_TRY(check_ptr(out, qn, "out"));
+      if (overlaps(out, qn * (d.dtype == BS_BF16 ? 2 : 4), merge->o_run, qn * 4))
+        return fail(BS_ERR_INVALID_ARG, "out overlaps o_run");
+    }
+  }
   BS_TRY(check_scale(scale));
   if (is_varlen(op)) BS_TRY(check_varlen_args(op, cu_q, cu_k, q_pos, k_pos, num_seqs, max_seqlen));
   const WsLayout L = layout_of(op, d, is_varlen(op) ? num_seqs : 1);
@@ -263,9 +281,11 @@ int fwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
   }
   ProfScope ps(BS_KERNEL_FWD, s);
   if (d.dtype == BS_BF16)
-    BS_HIP(launch_fwd_bf16(d, q, k, v, causal, scale, out, lse, ws, Lp, s), "forward launch");
+    BS_HIP(launch_fwd_bf16(d, q, k, v, causal, scale, out, lse, merge, ws, Lp, s),
+           "forward launch");
   else
-    BS_HIP(launch_fwd_f32(d, q, k, v, causal, scale, out, lse, ws, Lp, s), "forward launch");
+    BS_HIP(launch_fwd_f32(d, q, k, v, causal, scale, out, lse, merge, ws, Lp, s),
+           "forward launch");
   return ok();
 }
 
@@ -370,7 +390,7 @@ int bs_attn_varlen_fwd(const bs_dims* dims, const void* q, const void* k, const 
                        int32_t max_seqlen, int causal, float scale, void* out, float* lse,
                        void* workspace, size_t workspace_bytes, void* stream) {
   return fwd_common(BS_OP_VARLEN_FWD, dims, q, k, v, cu_seqlens_q, cu_seqlens_k, nullptr, nullptr,
-                    num_seqs, max_seqlen, 0, 0, causal, scale, out, lse, workspace,
+                    num_seqs, max_seqlen, 0, 0, causal, scale, out, lse, nullptr, workspace,
                     workspace_bytes, stream);
 }
 
@@ -389,7 +409,17 @@ int bs_attn_chunk_fwd(const bs_dims* dims, const void* q, const void* k, const v
                       void* out, float* lse, void* workspace, size_t workspace_bytes,
                       void* stream) {
   return fwd_common(BS_OP_CHUNK_FWD, dims, q, k, v, nullptr, nullptr, nullptr, nullptr, 1, 0,
-                    q_pos_offset, k_pos_offset, causal, scale, out, lse, workspace,
+                    q_pos_offset, k_pos_offset, causal, scale, out, lse, nullptr, workspace,
+                    workspace_bytes, stream);
+}
+
+int bs_attn_chunk_fwd_merge(const bs_dims* dims, const void* q, const void* k, const void* v,
+                            int64_t q_pos_offset, int64_t k_pos_offset, int causal, float scale,
+                            float* o_run, float* lse_run, int accumulate, void* out,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  const FwdMerge m{o_run, lse_run, accumulate != 0};
+  return fwd_common(BS_OP_CHUNK_FWD, dims, q, k, v, nullptr, nullptr, nullptr, nullptr, 1, 0,
+                    q_pos_offset, k_pos_offset, causal, scale, out, nullptr, &m, workspace,
                     workspace_bytes, stream);
 }
 
@@ -409,8 +439,21 @@ int bs_attn_packed_chunk_fwd(const bs_dims* dims, const void* q, const void* k, 
                              int32_t max_seqlen, int causal, float scale, void* out, float* lse,
                              void* workspace, size_t workspace_bytes, void* stream) {
   return fwd_common(BS_OP_PACKED_CHUNK_FWD, dims, q, k, v, cu_seqlens_q, cu_seqlens_k, q_pos,
-                    k_pos, num_seqs, max_seqlen, 0, 0, causal, scale, out, lse, workspace,
-                    workspace_bytes, stream);
+                    k_pos, num_seqs, max_seqlen, 0, 0, causal, scale, out, lse, nullptr,
+                    workspace, workspace_bytes, stream);
+}
+
+int bs_attn_packed_chunk_fwd_merge(const bs_dims* dims, const void* q, const void* k,
+                                   const void* v, const int32_t* cu_seqlens_q,
+                                   const int32_t* cu_seqlens_k, const int64_t* q_pos,
+                                   const int64_t* k_pos, int32_t num_seqs, int32_t max_seqlen,
+                                   int causal, float scale, float* o_run, float* lse_run,
+                                   int accumulate, void* out, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  const FwdMerge m{o_run, lse_run, accumulate != 0};
+  return fwd_common(BS_OP_PACKED_CHUNK_FWD, dims, q, k, v, cu_seqlens_q, cu_seqlens_k, q_pos,
+                    k_pos, num_seqs, max_seqlen, 0, 0, causal, scale, out, nullptr, &m,
+                    workspace, workspace_bytes, stream);
 }
 
 int bs_attn_packed_chunk_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,
@@ -450,6 +493,17 @@ int bs_lse_merge(const bs_dims* dims, const void* out_partials, const float* lse
   BS_HIP(launch_lse_merge(*dims, out_partials, lse_partials, n, out, lse,
                           static_cast<hipStream_t>(stream)),
          "merge launch");
+  return ok();
+}
+
+int bs_copy_async(void* dst, const void* src, size_t bytes, void* stream) {
+  if (bytes == 0) return ok();
+  if (dst == nullptr || src == nullptr) return fail(BS_ERR_INVALID_ARG, "dst or src is NULL");
+  if (bytes > (size_t)INT64_MAX || overlaps(dst, (int64_t)bytes, src, (int64_t)bytes))
+    return fail(BS_ERR_INVALID_ARG, "dst and src overlap");
+  BS_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDeviceNoCU,
+                        static_cast<hipStream_t>(stream)),
+         "DMA copy");
   return ok();
 }
 

@@ -218,9 +218,22 @@ hipError_t launch_plan(PlanKind kind, const int32_t* cu_q, const int32_t* cu_k,
                        int causal, int tile_a, int tile_b, int64_t max_items, void* ws,
                        const WsLayout& L, hipStream_t stream);
 
+// Forward epilogue that folds the step into a running result instead of writing
+// a partial (ring steps merged as they arrive): o_run float32 [T, hq, d], lse_run
+// [hq, T] natural log; accumulate = 0 replaces the running state, otherwise the
+// two are combined by their log-sum-exp weights.  With `out` non-null the merged
+// output goes there in the input dtype and o_run is not written.
+struct FwdMerge {
+  float* o_run;
+  float* lse_run;
+  int accumulate;
+};
+
+// merge == NULL: plain forward writing (out, lse)
 hipError_t launch_fwd_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
-                           int causal, float scale, void* out, float* lse, const void* ws,
-                           const WsLayout& L, hipStream_t stream);
+                           int causal, float scale, void* out, float* lse,
+                           const FwdMerge* merge, const void* ws, const WsLayout& L,
+                           hipStream_t stream);
 hipError_t launch_dq_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
                           const void* dout, const float* lse, const float* dvec, int causal,
                           float scale, void* dq, float* dq_acc, const void* ws, const WsLayout& L,
@@ -231,8 +244,8 @@ hipError_t launch_dkdv_bf16(const bs_dims& dims, const void* q, const void* k, c
                             const WsLayout& L, hipStream_t stream);
 
 hipError_t launch_fwd_f32(const bs_dims& dims, const void* q, const void* k, const void* v,
-                          int causal, float scale, void* out, float* lse, const void* ws,
-                          const WsLayout& L, hipStream_t stream);
+                          int causal, float scale, void* out, float* lse, const FwdMerge* merge,
+                          const void* ws, const WsLayout& L, hipStream_t stream);
 hipError_t launch_bwd_f32_dq(const bs_dims& dims, const void* q, const void* k, const void* v,
                              const float* lse, const void* dout, const float* dvec, int causal,
                              float scale, float* dq_acc, const void* ws, const WsLayout& L,

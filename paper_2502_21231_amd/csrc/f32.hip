@@ -20,6 +20,9 @@ struct F32Params {
   const float* dvec;
   float* o;
   float* lse_out;
+  float* o_run;    // forward running-merge mode (non-null): running output
+  float* lse_run;  // and its running LSE
+  int32_t accumulate;
   float* dq_acc;
   float* dk;
   float* dv;
@@ -101,13 +104,33 @@ __global__ __launch_bounds__(BM) void fwd_f32_kernel(const F32Params p) {
       for (int i = 0; i < D; ++i) acc[i] = fmaf(e, Vs[j * D + i], acc[i]);
     }
   }
-  if (valid) {
-    const float inv = l > 0.f ? 1.f / l : 0.f;
-    float* op = p.o + (int64_t)(it.a_start + r) * qs + (int64_t)h * D;
+  if (!valid) return;
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  const int64_t row = it.a_start + r;
+  const float lse2 = l > 0.f ? m + log2f(l) : -INFINITY;  // log2 domain
+  if (p.o_run == nullptr) {
+    float* op = p.o + row * qs + (int64_t)h * D;
 #pragma unroll
     for (int i = 0; i < D; ++i) op[i] = acc[i] * inv;
-    p.lse_out[(int64_t)h * p.total_q + it.a_start + r] = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
+    p.lse_out[(int64_t)h * p.total_q + row] = lse2 * kLn2;
+    return;
   }
+  // running merge: log-sum-exp weights of the running state and of this step
+  float* lr = p.lse_run + (int64_t)h * p.total_q + row;
+  const float old2 = p.accumulate ? *lr * kLog2e : -INFINITY;
+  const float mx = fmaxf(old2, lse2);
+  float w_old = 0.f, w_new = 0.f, lse_m = -INFINITY;
+  if (mx != -INFINITY) {
+    const float eo = fast_exp2(old2 - mx), en = fast_exp2(lse2 - mx);
+    w_old = eo / (eo + en);
+    w_new = en / (eo + en) * inv;
+    lse_m = (mx + log2f(eo + en)) * kLn2;
+  }
+  float* orun = p.o_run + row * qs + (int64_t)h * D;
+  float* dst = p.o != nullptr ? p.o + row * qs + (int64_t)h * D : orun;
+#pragma unroll
+  for (int i = 0; i < D; ++i) dst[i] = (w_old != 0.f ? orun[i] * w_old : 0.f) + acc[i] * w_new;
+  *lr = lse_m;
 }
 
 // dQ row of one query: sum over visible keys of dS_ij k_j, dS = P (dO.v_j - D).
@@ -256,8 +279,8 @@ F32Params make_params(const bs_dims& dims, const void* ws, const WsLayout& L, in
 }  // namespace
 
 hipError_t launch_fwd_f32(const bs_dims& dims, const void* q, const void* k, const void* v,
-                          int causal, float scale, void* out, float* lse, const void* ws,
-                          const WsLayout& L, hipStream_t stream) {
+                          int causal, float scale, void* out, float* lse, const FwdMerge* merge,
+                          const void* ws, const WsLayout& L, hipStream_t stream) {
   if (L.max_items == 0 || dims.hq == 0) return hipSuccess;
   F32Params p = make_params(dims, ws, L, causal, scale);
   p.q = static_cast<const float*>(q);
@@ -265,6 +288,9 @@ hipError_t launch_fwd_f32(const bs_dims& dims, const void* q, const void* k, con
   p.v = static_cast<const float*>(v);
   p.o = static_cast<float*>(out);
   p.lse_out = lse;
+  p.o_run = merge ? merge->o_run : nullptr;
+  p.lse_run = merge ? merge->lse_run : nullptr;
+  p.accumulate = merge ? merge->accumulate : 0;
   const dim3 grid((unsigned)(L.max_items * dims.hq));
   if (dims.head_dim == 128) hipLaunchKernelGGL(fwd_f32_kernel<128>, grid, dim3(BM), 0, stream, p);
   else hipLaunchKernelGGL(fwd_f32_kernel<64>, grid, dim3(BM), 0, stream, p);

@@ -41,6 +41,9 @@ struct FwdParams {
   const bf16* v;
   bf16* o;
   float* lse;
+  float* o_run;    // running-merge mode (non-null): float32 running output
+  float* lse_run;  // and its running LSE
+  int32_t accumulate;
   const WsHeader* hdr;
   const WorkItem* items;
   int64_t total_q;
@@ -194,8 +197,12 @@ void fwd_bf16_kernel(const FwdParams p) {
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  if (qvalid) {
-    bf16* op = p.o + (int64_t)(it.a_start + qrow) * qstride + (int64_t)h * D + hh * 4;
+  if (!qvalid) return;
+  const int64_t row = it.a_start + qrow;
+  const int64_t oidx = row * qstride + (int64_t)h * D + hh * 4;  // this lane's first column
+  const float lse2 = l_tot > 0.f ? m2 + log2f(l_tot) : -INFINITY;  // log2 domain
+  if (p.o_run == nullptr) {
+    bf16* op = p.o + oidx;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -205,17 +212,49 @@ void fwd_bf16_kernel(const FwdParams p) {
         *reinterpret_cast<bf16x4*>(op + db * 32 + a * 8) = x;
       }
     }
-    if (hh == 0)
-      p.lse[(int64_t)h * p.total_q + it.a_start + qrow] =
-          l_tot > 0.f ? (m2 + log2f(l_tot)) * kLn2 : -INFINITY;
+    if (hh == 0) p.lse[(int64_t)h * p.total_q + row] = lse2 * kLn2;
+    return;
   }
+  // Running merge: weights exp(LSE_old - LSE_new) and exp(LSE_step - LSE_new), which sum
+  // to one; a running LSE of -inf gives its O weight 0 without reading it.
+  float* lr = p.lse_run + (int64_t)h * p.total_q + row;
+  const float old2 = p.accumulate ? *lr * kLog2e : -INFINITY;
+  const float mx = fmaxf(old2, lse2);
+  float w_old = 0.f, w_new = 0.f, lse_m = -INFINITY;
+  if (mx != -INFINITY) {
+    const float eo = fast_exp2(old2 - mx), en = fast_exp2(lse2 - mx);
+    const float rs = 1.f / (eo + en);
+    w_old = eo * rs;
+    w_new = en * rs * inv;
+    lse_m = (mx + log2f(eo + en)) * kLn2;
+  }
+  float* orun = p.o_run + oidx;
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      f32x4 x = {oacc[db][a * 4 + 0] * w_new, oacc[db][a * 4 + 1] * w_new,
+                 oacc[db][a * 4 + 2] * w_new, oacc[db][a * 4 + 3] * w_new};
+      if (w_old != 0.f) {
+        const f32x4 prev = *reinterpret_cast<const f32x4*>(orun + db * 32 + a * 8);
+        x = prev * w_old + x;
+      }
+      if (p.o != nullptr)
+        *reinterpret_cast<bf16x4*>(p.o + oidx + db * 32 + a * 8) =
+            bf16x4{f2bf(x[0]), f2bf(x[1]), f2bf(x[2]), f2bf(x[3])};
+      else
+        *reinterpret_cast<f32x4*>(orun + db * 32 + a * 8) = x;
+    }
+  }
+  if (hh == 0) *lr = lse_m;
 }
 
 }  // namespace
 
 hipError_t launch_fwd_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
-                           int causal, float scale, void* out, float* lse, const void* ws,
-                           const WsLayout& L, hipStream_t stream) {
+                           int causal, float scale, void* out, float* lse,
+                           const FwdMerge* merge, const void* ws, const WsLayout& L,
+                           hipStream_t stream) {
   if (L.max_items == 0 || dims.hq == 0) return hipSuccess;
   FwdParams p;
   p.q = static_cast<const bf16*>(q);
@@ -223,6 +262,9 @@ hipError_t launch_fwd_bf16(const bs_dims& dims, const void* q, const void* k, co
   p.v = static_cast<const bf16*>(v);
   p.o = static_cast<bf16*>(out);
   p.lse = lse;
+  p.o_run = merge ? merge->o_run : nullptr;
+  p.lse_run = merge ? merge->lse_run : nullptr;
+  p.accumulate = merge ? merge->accumulate : 0;
   p.hdr = static_cast<const WsHeader*>(ws);
   p.items = reinterpret_cast<const WorkItem*>(static_cast<const char*>(ws) + L.sorted);
   p.total_q = dims.total_q;

@@ -27,7 +27,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 14, names
+    assert len(names) == 17, names
     assert set(names) == set(B.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
@@ -74,6 +74,43 @@ def test_rejects_bad_arguments_without_device(lib):
                                         1 << 30, None) == B.BS_ERR_INVALID_ARG
     assert "dq_accum" in B.bs_last_error()
     assert lib.bs_read_device_status(None, None) == B.BS_ERR_WORKSPACE
+    assert lib.bs_copy_async(None, FAKE, 64, None) == B.BS_ERR_INVALID_ARG
+    assert lib.bs_copy_async(FAKE, FAKE + 32, 64, None) == B.BS_ERR_INVALID_ARG
+    assert "overlap" in B.bs_last_error()
+    assert lib.bs_copy_async(None, None, 0, None) == B.BS_OK  # nothing to copy: nothing enqueued
+
+
+def test_running_merge_rejects_bad_state(lib):
+    """The forward steps that fold into a running (O, LSE) need both running buffers; the
+    optional final output must not overlap the running O."""
+    d = dims()
+    qn = 128 * 4 * 128  # total_q * hq * head_dim
+
+    def chunk(o_run=FAKE, lse_run=FAKE, out=None, ws_bytes=1 << 30):
+        return lib.bs_attn_chunk_fwd_merge(ctypes.byref(d), FAKE, FAKE, FAKE, 0, 0, 1, 0.1, o_run,
+                                           lse_run, 1, out, FAKE, ws_bytes, None)
+
+    assert chunk(o_run=None) == B.BS_ERR_INVALID_ARG
+    assert "o_run is NULL" in B.bs_last_error()
+    assert chunk(lse_run=None) == B.BS_ERR_INVALID_ARG
+    assert "lse_run is NULL" in B.bs_last_error()
+    assert chunk(o_run=FAKE + 8) == B.BS_ERR_INVALID_ARG
+    assert "aligned" in B.bs_last_error()
+    # bf16 out of qn * 2 bytes starting inside the float32 o_run, or o_run starting inside out
+    assert chunk(o_run=1 << 20, out=(1 << 20) + qn * 4 - 16) == B.BS_ERR_INVALID_ARG
+    assert "overlaps" in B.bs_last_error()
+    assert chunk(o_run=(1 << 20) + qn * 2 - 16, out=1 << 20) == B.BS_ERR_INVALID_ARG
+    # adjacent buffers pass that check and stop at the (too small) workspace, enqueueing nothing
+    assert chunk(o_run=1 << 20, out=(1 << 20) + qn * 4, ws_bytes=16) == B.BS_ERR_WORKSPACE
+    assert chunk(o_run=(1 << 20) + qn * 2, out=1 << 20, ws_bytes=16) == B.BS_ERR_WORKSPACE
+    assert lib.bs_attn_packed_chunk_fwd_merge(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                              FAKE, 1, 128, 1, 0.1, FAKE, FAKE, 0, None, FAKE,
+                                              1 << 30, None) == B.BS_ERR_INVALID_ARG
+    assert "q_pos" in B.bs_last_error()
+    assert lib.bs_attn_packed_chunk_fwd_merge(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                              FAKE, 1, 128, 1, 0.1, None, FAKE, 0, None, FAKE,
+                                              1 << 30, None) == B.BS_ERR_INVALID_ARG
+    assert "o_run is NULL" in B.bs_last_error()
 
 
 def test_workspace_size_grows_with_problem(lib):

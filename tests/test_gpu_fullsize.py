@@ -109,9 +109,12 @@ def test_gqa_70b_131k_mixed_seed0(gpu):
     varlen_fullsize(inputs.mixed_long_short_lengths(0), 64, 8, 0)
 
 
-def chunk_share(hq, hkv, q_offs, kv_offs, pairs, seed, c=32768):
+def chunk_share(hq, hkv, q_offs, kv_offs, pairs, seed, c=32768, ring=False):
     """A context-parallel share: per-step chunk forward, LSE merge, per-step chunk backward with
-    dQ (and, for KV parts seen by several Q parts, dK/dV) accumulated in float32."""
+    dQ (and, for KV parts seen by several Q parts, dK/dV) accumulated in float32.  With ring=True
+    (one Q part) the share runs through the single-GPU ring rehearsal instead, as the benchmark
+    times it: shards received on a copy stream, every forward step folded into a running (O, LSE)
+    in the kernel epilogue, dK/dV sent out on the copy stream."""
     G = hq // hkv
     Q = [gen(seed, inputs.TID_Q + 100 * i, (c, hq, D)) for i in range(len(q_offs))]
     dO = [gen(seed, inputs.TID_DO + 100 * i, (c, hq, D)) for i in range(len(q_offs))]
@@ -121,6 +124,22 @@ def chunk_share(hq, hkv, q_offs, kv_offs, pairs, seed, c=32768):
     Kg, Vg = [t.cuda() for t in K], [t.cuda() for t in V]
     per_q = {i: [j for (a, j) in pairs if a == i] for i in range(len(q_offs))}
     multi = any(sum(1 for (_, b) in pairs if b == j) > 1 for j in range(len(kv_offs)))
+    if ring:
+        from paper_2502_21231_amd.ring import ChunkRing
+        assert len(q_offs) == 1 and not multi
+        order = sorted(per_q[0], key=lambda j: -kv_offs[j])
+        r = ChunkRing(Qg[0], dOg[0], [Kg[j] for j in order], [Vg[j] for j in order], q_offs[0],
+                      [kv_offs[j] for j in order], True, SCALE)
+        for _ in range(2):  # a second pass reuses every buffer and event of the first
+            o, l = r.forward()
+            dq, dks, dvs = r.backward()
+        torch.cuda.synchronize()
+        dK, dV = [None] * len(kv_offs), [None] * len(kv_offs)
+        for s, j in enumerate(order):
+            dK[j], dV[j] = dks[s].cpu(), dvs[s].cpu()
+        chunk_share_check(Q, dO, K, V, [o.cpu()], [l.cpu()], [dq.cpu()], dK, dV, hq, hkv, q_offs,
+                          kv_offs, pairs, seed, c)
+        return
     O, L = [], []
     for i in range(len(q_offs)):
         po, pl = zip(*[B.bs_attn_chunk_fwd(Qg[i], Kg[j], Vg[j], q_offs[i], kv_offs[j], True, SCALE)
@@ -141,7 +160,13 @@ def chunk_share(hq, hkv, q_offs, kv_offs, pairs, seed, c=32768):
         dV = [B.bs_dq_finalize(t, torch.empty(c, hkv, D, dtype=BF, device="cuda")) for t in dV]
     torch.cuda.synchronize()
     O, L, dQ, dK, dV = ([t.cpu() for t in x] for x in (O, L, dQ, dK, dV))
+    chunk_share_check(Q, dO, K, V, O, L, dQ, dK, dV, hq, hkv, q_offs, kv_offs, pairs, seed, c)
 
+
+def chunk_share_check(Q, dO, K, V, O, L, dQ, dK, dV, hq, hkv, q_offs, kv_offs, pairs, seed, c):
+    """Sampled rows of O, LSE, dQ and the last keys' dK, dV against the oracle; gradient sums."""
+    G = hq // hkv
+    per_q = {i: [j for (a, j) in pairs if a == i] for i in range(len(q_offs))}
     rng = np.random.default_rng(seed + 2000)
     heads = sorted({0, hq - 1, int(rng.integers(0, hq))})
     for i in range(len(q_offs)):
@@ -193,6 +218,14 @@ def test_cp_share_7b_2048k(gpu):
     """A 32768-token Q chunk at 1015808 against 8 KV chunks at (24..31)*32768, 32/32 heads."""
     c = 32768
     chunk_share(32, 32, [1015808], [(24 + i) * c for i in range(8)], [(0, j) for j in range(8)], 0)
+
+
+def test_cp_ring_7b_2048k(gpu):
+    """The same share through the ring rehearsal that the benchmark times (fused running merge,
+    shards and gradients moved on a copy stream), two passes."""
+    c = 32768
+    chunk_share(32, 32, [1015808], [(24 + i) * c for i in range(8)], [(0, j) for j in range(8)], 0,
+                ring=True)
 
 
 def test_zigzag_share_141b_256k(gpu):

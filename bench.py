@@ -29,7 +29,7 @@ BF16_PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12   # 2516.6: MI355X dense bf16 MFMA 
 REPO = os.path.dirname(os.path.abspath(__file__))
 # sources whose text fixes each timed kernel (a counter record applies only to them)
 KERNEL_SOURCES = {"fwd": ["fwd_bf16.hip", "common.hpp"], "bwd_dq": ["bwd_bf16.hip", "common.hpp"],
-                  "bwd_dkdv": ["bwd_bf16.hip", "common.hpp"]}
+                  "bwd_dkdv": ["bwd_bf16.hip", "common.hpp"], "xent": ["xent.hip", "common.hpp"]}
 
 
 def kernel_source_hash(kernel):
@@ -74,6 +74,10 @@ WORKLOADS = {
                  "every forward step folded into a running float32 (O, LSE) in the kernel epilogue "
                  "(no partials, no merge pass); the backward receives the shards the same way and "
                  "sends each shard's dK, dV out on the copy stream",
+    "xent_llama3_256k": "fused softmax cross-entropy fwd+bwd (loss, lse and the bf16 gradient of "
+                        "bf16 logits) over 262144 tokens x a 128256-entry vocabulary (LLaMA3), "
+                        "logits N(0, 3^2), labels uniform, ~1/1024 ignored; the gradient is "
+                        "scaled by 1/(valid tokens) and written to its own buffer",
     "zigzag141b": "141B-shaped zig-zag CP share: 48 q heads, 8 kv heads, Q halves of 32768 at 0 "
                   "and 229376 against the matching KV halves, fwd + merge + bwd",
     "zigzag_packed7b": "7B-shaped packed CP share (dist-attn with packing): device 0 of a 4-way "
@@ -436,6 +440,81 @@ def run_zigzag_packed_bench(args, dev):
     return res
 
 
+XENT = dict(rows=262144, vocab=128256, cpu_rows=16384)
+
+
+def run_xent_bench(args, dev):
+    """The fused cross-entropy: whole-call HIP events on the library's stream, the kernel's own
+    events from the profiling hooks; HBM bytes counted algorithmically (logits read once, gradient
+    written once, labels, loss, lse)."""
+    import torch
+    from paper_2502_21231_amd import bs_attn as B
+    from paper_2502_21231_amd import inputs
+    T, V = XENT["rows"], XENT["vocab"]
+    z, y = inputs.xent_inputs(args.seed, T, V, device=dev)
+    n_valid = int((y != -100).sum())
+    g = 1.0 / n_valid
+    loss = torch.empty(T, dtype=torch.float32, device=dev)
+    lse = torch.empty(T, dtype=torch.float32, device=dev)
+    dz = torch.empty_like(z)
+
+    def step():
+        B.bs_softmax_xent(z, y, -100, g, loss, lse, dz)
+
+    for _ in range(args.warmup):
+        step()
+    s = torch.cuda.current_stream(dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize(dev)
+    B.bs_set_profiling(True)
+    ev[0].record(s)
+    for i in range(args.steps):
+        step()
+        ev[i + 1].record(s)
+    torch.cuda.synchronize(dev)
+    k_ms, k_n = B.bs_profile_read(B.BS_KERNEL_XENT)
+    B.bs_set_profiling(False)
+    total_ms = ev[0].elapsed_time(ev[-1])
+    per = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
+    ms = total_ms / args.steps
+    nbytes = 2 * T * V * z.element_size() + T * 8 + 2 * T * 4
+    kern_ms = k_ms / k_n
+    res = {
+        "metric": "fused softmax cross-entropy fwd+bwd, algorithmic HBM GB/s, 1 GPU",
+        "value": nbytes / (ms * 1e-3) / 1e9, "unit": "GB/s", "ms_per_step": ms,
+        "ms_per_step_median": per[len(per) // 2], "dtype": "bf16",
+        "config": {"workload": WORKLOADS[args.workload], "rows": T, "vocab": V, "valid_rows": n_valid,
+                   "seed": args.seed, "bytes_per_step": nbytes},
+        "kernels": {"xent": {"ms_per_step": k_ms / args.steps, "launches_per_step": k_n / args.steps,
+                             "avg_ms_per_launch": kern_ms}},
+        "roofline": {"kernel": "bs_softmax_xent (bf16, fused gradient)", "bound": "hbm",
+                     "achieved": nbytes / (kern_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": nbytes / (kern_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                     "traffic": recorded_traffic(args.workload, "xent")},
+    }
+    if args.cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_xent(z, y, g)
+    return res
+
+
+def cpu_baseline_xent(z, y, g):
+    """The float64 oracle on the first rows of the same logits (a bounded sample), as GB/s of the
+    same algorithmic bytes per row."""
+    from oracle.xent import softmax_xent
+    R, blk = XENT["cpu_rows"], 2048  # blocks of rows bound the oracle's float64 temporaries
+    dt = 0.0
+    for r0 in range(0, R, blk):
+        zc, yc = z[r0:r0 + blk].cpu(), y[r0:r0 + blk].cpu().numpy()
+        t0 = time.perf_counter()
+        softmax_xent(zc, yc, -100, g)
+        dt += time.perf_counter() - t0
+    V = z.shape[1]
+    nbytes = 2 * R * V * z.element_size() + R * 8 + 2 * R * 4
+    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"rows 0..{R - 1} of {z.shape[0]} (all {V} vocabulary entries), float64 NumPy "
+                      f"(element-wise, one thread), in blocks of {blk} rows: {dt:.1f} s", "seconds": dt}
+
+
 def visible_pairs_chunk_closed(lq, lk, diag):
     """Exact visible (query, key) pairs of a chunk pair: key j visible to query i iff j - i <= diag."""
     tot = 0
@@ -489,6 +568,16 @@ def main():
         res = run_zigzag_packed_bench(args, dev)
     elif args.workload == "cp7b_ring":
         res = run_cp_ring_bench(args, dev)
+    elif args.workload == "xent_llama3_256k":
+        res = run_xent_bench(args, dev)
+        line = {"metric": res["metric"], "value": round(res["value"], 3), "unit": res["unit"], "n_gpus": 1,
+                "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(res["ms_per_step"], 4),
+                "ms_per_step_median": round(res["ms_per_step_median"], 4), "higher_is_better": True,
+                "scaling": "weak", "vs_baseline": None, "dtype": res["dtype"], "data": "synthetic",
+                "config": res["config"], "kernels": res["kernels"], "roofline": res["roofline"],
+                "cpu_baseline": res.get("cpu_baseline")}
+        print(json.dumps(line), flush=True)
+        return
     else:
         res = run_chunk_bench(args, dev)
     line = {

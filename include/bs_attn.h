@@ -251,6 +251,25 @@ int bs_lse_merge(const bs_dims* dims, const void* out_partials, const float* lse
  * enqueues nothing. */
 int bs_copy_async(void* dst, const void* src, size_t bytes, void* stream);
 
+/* Softmax cross-entropy of next-token prediction with its gradient fused in (Sec. 7,
+ * Fused SoftmaxCrossEntropy: bf16 logits over a vocabulary of ~128K entries, the
+ * arithmetic in fp32, no fp32 copy of the logits).  logits: [rows, vocab] of `dtype`
+ * (BS_BF16 or BS_F32), row-major; labels: int64 [rows].  Per row i:
+ *   lse_i  = log sum_j exp(z_ij)                      (float32, natural log)
+ *   loss_i = lse_i - z_i,label_i                      (float32; 0 if label_i == ignore_index)
+ *   dlogits_ij = grad_scale * (exp(z_ij - lse_i) - [j == label_i])   (in `dtype`, RNE)
+ * grad_scale is the upstream gradient of every token's loss (1/N for the token-level loss of
+ * Sec. 5.1, Loss and Model Update).  An ignored row's gradient is all zero; its lse is still
+ * written.  A label outside [0, vocab) that is not ignore_index gives loss NaN and the row's
+ * gradient without the one-hot term (nothing is read or written outside the row).  A row
+ * whose logits are all -inf gives lse -inf and loss NaN.  lse may be NULL (not written);
+ * dlogits may be NULL (loss only), may equal logits (gradient written in place), and must not
+ * otherwise overlap it.  1 <= vocab < 2^31 and 0 <= rows < 2^30.  The result is bitwise
+ * deterministic. */
+int bs_softmax_xent(int64_t rows, int64_t vocab, int dtype, const void* logits,
+                    const int64_t* labels, int64_t ignore_index, float grad_scale, float* loss,
+                    float* lse, void* dlogits, void* stream);
+
 /* TEST HELPER (synchronises `stream`): the device status word left in the
  * workspace by the last planning kernel; BS_OK, or BS_ERR_DEVICE_STATUS with
  * the BS_DEV_* code in bs_last_error(). */
@@ -281,7 +300,8 @@ enum {
   BS_KERNEL_BWD_DKDV = 4,   /* backward kernel producing dK and dV */
   BS_KERNEL_FINALIZE = 5,   /* float32 dQ accumulator -> dq */
   BS_KERNEL_MERGE = 6,      /* LSE merge */
-  BS_KERNEL_COUNT = 7
+  BS_KERNEL_XENT = 7,       /* softmax cross-entropy */
+  BS_KERNEL_COUNT = 8
 };
 
 /* Profiling (off by default, process-wide).  While enabled, every call

@@ -26,11 +26,12 @@ EXPORTS = (
     "bs_attn_workspace_size", "bs_attn_varlen_fwd", "bs_attn_varlen_bwd", "bs_attn_chunk_fwd",
     "bs_attn_chunk_bwd", "bs_attn_packed_chunk_fwd", "bs_attn_packed_chunk_bwd",
     "bs_attn_chunk_fwd_merge", "bs_attn_packed_chunk_fwd_merge", "bs_copy_async",
+    "bs_softmax_xent",
     "bs_dq_finalize", "bs_lse_merge", "bs_read_device_status",
     "bs_attn_plan_export", "bs_set_profiling", "bs_profile_read", "bs_last_error",
 )
 (BS_KERNEL_PLAN, BS_KERNEL_FWD, BS_KERNEL_PREPROCESS, BS_KERNEL_BWD_DQ, BS_KERNEL_BWD_DKDV,
- BS_KERNEL_FINALIZE, BS_KERNEL_MERGE) = range(7)
+ BS_KERNEL_FINALIZE, BS_KERNEL_MERGE, BS_KERNEL_XENT) = range(8)
 
 
 class BsError(RuntimeError):
@@ -81,6 +82,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "bs_dq_finalize": (ctypes.c_int, [_DIMS, _P, _P, _P]),
         "bs_lse_merge": (ctypes.c_int, [_DIMS, _P, _P, _I32, _P, _P, _P]),
         "bs_copy_async": (ctypes.c_int, [_P, _P, _SZ, _P]),
+        "bs_softmax_xent": (ctypes.c_int, [_I64, _I64, ctypes.c_int, _P, _P, _I64, _F, _P, _P, _P, _P]),
         "bs_read_device_status": (ctypes.c_int, [_P, _P]),
         "bs_attn_plan_export": (ctypes.c_int, [ctypes.c_int, _DIMS, _P, _P, _I32, _I32, _I64, _I64,
                                                _P, _P, ctypes.c_int, _P, _SZ, _P, _SZ,
@@ -417,6 +419,35 @@ def bs_copy_async(dst, src):
     _check(load_library().bs_copy_async(_ptr(dst), _ptr(src), src.numel() * src.element_size(),
                                         _stream(src.device)))
     return dst
+
+
+def bs_softmax_xent(logits, labels, ignore_index: int = -100, grad_scale: float = 1.0,
+                    loss=None, lse=None, dlogits=None, with_grad: bool = True):
+    """Per-token cross-entropy of logits [T, V] (bf16 or float32) against int64 labels [T], with
+    the fused gradient grad_scale * (softmax - onehot).  dlogits: a new tensor (default), a
+    given one, or `logits` itself for an in-place gradient; with_grad=False computes the loss
+    only.  Returns (loss float32 [T], lse float32 [T], dlogits or None)."""
+    _need(logits, "logits", ndim=2)
+    _need(labels, "labels", torch.int64, 1)
+    T, V = logits.shape
+    if labels.shape[0] != T:
+        raise ValueError("one label per row of logits")
+    dev = logits.device
+    loss = torch.empty(T, dtype=torch.float32, device=dev) if loss is None else loss
+    lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
+    _need(loss, "loss", torch.float32, 1)
+    _need(lse, "lse", torch.float32, 1)
+    if with_grad:
+        dlogits = torch.empty_like(logits) if dlogits is None else dlogits
+        _need(dlogits, "dlogits", logits.dtype, 2)
+        if dlogits.shape != logits.shape:
+            raise ValueError("dlogits must have the shape of logits")
+    else:
+        dlogits = None
+    _check(load_library().bs_softmax_xent(T, V, _dtype_code(logits), _ptr(logits), _ptr(labels),
+                                          int(ignore_index), float(grad_scale), _ptr(loss), _ptr(lse),
+                                          _ptr(dlogits), _stream(dev)))
+    return loss, lse, dlogits
 
 
 def bs_read_device_status(workspace) -> int:

@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libbs_attn.so")
 
-SOURCES = ["plan.hip", "fwd_bf16.hip", "bwd_bf16.hip", "f32.hip", "rowwise.hip", "capi.hip"]
+SOURCES = ["plan.hip", "fwd_bf16.hip", "bwd_bf16.hip", "f32.hip", "rowwise.hip", "xent.hip", "capi.hip"]
 
 ARCH = "gfx950"
 CFLAGS = [

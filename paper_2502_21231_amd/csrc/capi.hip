@@ -507,6 +507,33 @@ int bs_copy_async(void* dst, const void* src, size_t bytes, void* stream) {
   return ok();
 }
 
+int bs_softmax_xent(int64_t rows, int64_t vocab, int dtype, const void* logits,
+                    const int64_t* labels, int64_t ignore_index, float grad_scale, float* loss,
+                    float* lse, void* dlogits, void* stream) {
+  if (dtype != BS_F32 && dtype != BS_BF16)
+    return fail(BS_ERR_UNSUPPORTED, "dtype %d is not BS_F32 or BS_BF16", dtype);
+  if (rows < 0 || rows >= kMaxTokens)
+    return fail(BS_ERR_INVALID_ARG, "rows = %lld out of [0, 2^30)", (long long)rows);
+  if (vocab < 1 || vocab > INT32_MAX)
+    return fail(BS_ERR_INVALID_ARG, "vocab = %lld out of [1, 2^31)", (long long)vocab);
+  if (!isfinite(grad_scale)) return fail(BS_ERR_INVALID_ARG, "grad_scale must be finite");
+  if (rows == 0) return ok();
+  if (logits == nullptr || labels == nullptr || loss == nullptr)
+    return fail(BS_ERR_INVALID_ARG, "logits, labels or loss is NULL");
+  const int64_t esize = dtype == BS_BF16 ? 2 : 4;
+  if (reinterpret_cast<uintptr_t>(logits) % esize != 0 ||
+      (dlogits != nullptr && reinterpret_cast<uintptr_t>(dlogits) % esize != 0))
+    return fail(BS_ERR_INVALID_ARG, "logits / dlogits not aligned to their element size");
+  const int64_t nbytes = rows * vocab * esize;
+  if (dlogits != nullptr && dlogits != logits && overlaps(dlogits, nbytes, logits, nbytes))
+    return fail(BS_ERR_INVALID_ARG, "dlogits overlaps logits without being equal to it");
+  ProfScope ps(BS_KERNEL_XENT, static_cast<hipStream_t>(stream));
+  BS_HIP(launch_softmax_xent(rows, vocab, dtype, logits, labels, ignore_index, grad_scale, loss,
+                             lse, dlogits, static_cast<hipStream_t>(stream)),
+         "cross-entropy launch");
+  return ok();
+}
+
 int bs_read_device_status(const void* workspace, void* stream) {
   if (workspace == nullptr) return fail(BS_ERR_WORKSPACE, "workspace is NULL");
   WsHeader h;

@@ -262,4 +262,7 @@ hipError_t launch_dq_finalize(const bs_dims& dims, const float* dq_acc, void* dq
                               const void* ws, hipStream_t stream);
 hipError_t launch_lse_merge(const bs_dims& dims, const void* out_parts, const float* lse_parts,
                             int32_t n, void* out, float* lse, hipStream_t stream);
+hipError_t launch_softmax_xent(int64_t rows, int64_t vocab, int dtype, const void* logits,
+                               const int64_t* labels, int64_t ignore_index, float grad_scale,
+                               float* loss, float* lse, void* dlogits, hipStream_t stream);
 }  // namespace bs

@@ -2,8 +2,8 @@
 
 This module only draws numbers and lays out indices: sequence-length mixes
 shaped after the paper's long-tailed datasets (Sec. 3.1, Observation 1, and the
-skew it reports), i.i.d. N(0,1) tensors, and the token bookkeeping of the
-zig-zag packing layout (Sec. 7).  It holds none of the attention arithmetic, and
+skew it reports), i.i.d. N(0,1) tensors, the token bookkeeping of the zig-zag
+packing layout (Sec. 7), and logits with labels for the cross-entropy.  It holds none of the attention arithmetic, and
 it imports neither the HIP binding nor the oracle.
 
 Tensors are drawn as float32 from ``numpy.random.default_rng([seed, tensor_id,
@@ -55,6 +55,37 @@ def normal(seed: int, tensor_id: int, shape, dtype: torch.dtype = torch.bfloat16
             list(ex.map(fill, range(nchunks)))
     t = torch.from_numpy(out).reshape(tuple(shape))
     return t if dtype == torch.float32 else t.to(dtype)
+
+
+TID_LOGITS, TID_LABELS = 40, 41
+
+
+def xent_inputs(seed: int, rows: int, vocab: int, std: float = 3.0, dtype=torch.bfloat16,
+                ignore_every: int = 1024, ignore_index: int = -100, device=None):
+    """Logits [rows, vocab] ~ N(0, std^2) in `dtype` and int64 labels uniform in [0, vocab),
+    about one row in `ignore_every` labelled ignore_index (the last token of a packed sequence
+    has no next token).  With `device` (a GPU) the values are drawn there by torch's seeded
+    Philox generator, chunk by chunk of rows, which keeps a 256K x 128K matrix off the host;
+    without it they come from the CPU generator of normal().  Either way the same (seed,
+    shape, device type) gives the same values."""
+    if device is None:
+        z = normal(seed, TID_LOGITS, (rows, vocab), torch.float32) * std
+        rng = np.random.default_rng([seed, TID_LABELS])
+        y = rng.integers(0, vocab, rows)
+        y[rng.random(rows) < 1.0 / ignore_every] = ignore_index
+        return z.to(dtype), torch.from_numpy(y)
+    g = torch.Generator(device=device)
+    z = torch.empty(rows, vocab, dtype=dtype, device=device)
+    step = max(1, (1 << 28) // max(vocab, 1))  # rows per draw: 256 Mi float32 of scratch at most
+    for r0 in range(0, rows, step):
+        g.manual_seed(seed * 1000003 + TID_LOGITS * 7919 + r0)
+        r1 = min(rows, r0 + step)
+        z[r0:r1] = (torch.randn(r1 - r0, vocab, generator=g, device=device) * std).to(dtype)
+    g.manual_seed(seed * 1000003 + TID_LABELS * 7919)
+    y = torch.randint(0, vocab, (rows,), generator=g, device=device, dtype=torch.int64)
+    drop = torch.rand(rows, generator=g, device=device) < 1.0 / ignore_every
+    y[drop] = ignore_index
+    return z, y
 
 
 def cu_seqlens(lengths) -> np.ndarray:

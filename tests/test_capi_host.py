@@ -27,7 +27,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 17, names
+    assert len(names) == 18, names
     assert set(names) == set(B.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
@@ -78,6 +78,28 @@ def test_rejects_bad_arguments_without_device(lib):
     assert lib.bs_copy_async(FAKE, FAKE + 32, 64, None) == B.BS_ERR_INVALID_ARG
     assert "overlap" in B.bs_last_error()
     assert lib.bs_copy_async(None, None, 0, None) == B.BS_OK  # nothing to copy: nothing enqueued
+
+
+def test_softmax_xent_rejects_bad_arguments(lib):
+    def xent(rows=4, vocab=1000, dtype=B.BS_BF16, logits=FAKE, labels=FAKE, g=1.0, loss=FAKE,
+             dlogits=None):
+        return lib.bs_softmax_xent(rows, vocab, dtype, logits, labels, -100, g, loss, None,
+                                   dlogits, None)
+
+    assert xent(dtype=5) == B.BS_ERR_UNSUPPORTED
+    assert xent(rows=-1) == B.BS_ERR_INVALID_ARG
+    assert xent(rows=1 << 30) == B.BS_ERR_INVALID_ARG
+    assert xent(vocab=0) == B.BS_ERR_INVALID_ARG
+    assert xent(vocab=1 << 31) == B.BS_ERR_INVALID_ARG
+    assert xent(g=float("inf")) == B.BS_ERR_INVALID_ARG
+    assert xent(logits=None) == B.BS_ERR_INVALID_ARG
+    assert xent(loss=None) == B.BS_ERR_INVALID_ARG
+    assert xent(logits=FAKE + 1) == B.BS_ERR_INVALID_ARG  # bf16 needs 2-byte alignment
+    assert "aligned" in B.bs_last_error()
+    # a gradient buffer that overlaps the logits without being them
+    assert xent(dlogits=FAKE + 64) == B.BS_ERR_INVALID_ARG
+    assert "overlaps" in B.bs_last_error()
+    assert xent(rows=0, logits=None, labels=None, loss=None) == B.BS_OK  # nothing to do
 
 
 def test_running_merge_rejects_bad_state(lib):

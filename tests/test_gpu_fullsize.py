@@ -320,3 +320,40 @@ def test_zigzag_packed_7b_fullsize(gpu):
     tol = 0.02 * math.sqrt(n) + 1e-3 * float(so.abs().max())
     assert float(sk.abs().max()) <= tol, ("sum dK", float(sk.abs().max()), tol)
     assert float((sv - so).abs().max()) <= tol, ("sum dV", float((sv - so).abs().max()), tol)
+
+
+def test_xent_llama3_256k_fullsize(gpu):
+    """The benchmark's cross-entropy call: 262144 tokens x 128256 vocabulary, bf16 logits (67 GB)
+    and gradient (67 GB).  16 sampled rows against the oracle (tolerances of test_gpu_xent), and
+    over every row: ignored rows give loss 0 and a zero gradient, every other row a finite loss
+    >= 0, and its gradient sums to zero up to the bf16 rounding of its entries (each off by at
+    most 2^-9 of itself: |sum| <= 2^-9 * sum |dz| = 2^-8 g)."""
+    from oracle.xent import softmax_xent
+    T, V = 262144, 128256
+    z, y = inputs.xent_inputs(0, T, V, device="cuda")
+    valid = y != -100
+    g = 1.0 / int(valid.sum())
+    loss, lse, dz = B.bs_softmax_xent(z, y, -100, g)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(77)
+    rows = sorted({0, 1, T // 2, T - 1} | {int(r) for r in rng.integers(0, T, 12)})
+    ign = int(torch.nonzero(~valid)[0])
+    rows.append(ign)
+    for r in rows:
+        zr, yr = z[r:r + 1].cpu(), y[r:r + 1].cpu().numpy()
+        l_ref, s_ref, d_ref = softmax_xent(zr, yr, -100, g)
+        check_close(f"loss row {r}", f64(loss[r:r + 1]), l_ref, 5e-5)
+        check_close(f"lse row {r}", f64(lse[r:r + 1]), s_ref, 5e-5)
+        check_close(f"dlogits row {r}", f64(dz[r:r + 1]), d_ref, g * 1e-4, True)
+    assert bool((loss[~valid] == 0).all())
+    lv = loss[valid]
+    assert bool(torch.isfinite(lv).all()) and bool((lv >= 0).all())
+    for r0 in range(0, T, 4096):
+        part = dz[r0:r0 + 4096].float()
+        sums = part.sum(dim=1)
+        v = valid[r0:r0 + 4096]
+        assert bool((sums[v].abs() <= g * (2.0 ** -8 + 1e-4)).all()), r0
+        assert not bool(part[~v].any()), r0
+        del part
+    del z, dz
+    torch.cuda.empty_cache()

@@ -74,6 +74,12 @@ WORKLOADS = {
                  "every forward step folded into a running float32 (O, LSE) in the kernel epilogue "
                  "(no partials, no merge pass); the backward receives the shards the same way and "
                  "sends each shard's dK, dV out on the copy stream",
+    "hdp_batch7b": "HDP planning checked on the GPU: a 524288-token global batch of log-normal "
+                   "lengths (median 1K, clipped to [128, 128K]) planned for 16 ranks of 8K tokens "
+                   "by the native Alg. 1 / Alg. 2 planners with T(s) fitted from this library's "
+                   "measured attention; a step runs the attention fwd+bwd (7B shape: 32/32 heads, "
+                   "head_dim 128) of every micro-batch of the DP-Balance plan (a context-parallel "
+                   "sequence once, whole)",
     "xent_llama3_256k": "fused softmax cross-entropy fwd+bwd (loss, lse and the bf16 gradient of "
                         "bf16 logits) over 262144 tokens x a 128256-entry vocabulary (LLaMA3), "
                         "logits N(0, 3^2), labels uniform, ~1/1024 ignored; the gradient is "
@@ -441,6 +447,177 @@ def run_zigzag_packed_bench(args, dev):
 
 
 XENT = dict(rows=262144, vocab=128256, cpu_rows=16384)
+HDP = dict(total=524288, capacity=8192, ranks=16, max_len=131072, hq=32, hkv=32, d=128,
+           fit_lengths=[1024, 2048, 4096, 8192, 16384, 32768, 65536], layers=32,
+           act_bytes_per_token=34 * 4096, delta=1e-4, buckets=4)
+
+
+def _varlen_call(q, k, v, do, cu, maxlen, ws_f, ws_b, out, lse, dq, dk, dv, scale):
+    from paper_2502_21231_amd import bs_attn as B
+    B.bs_attn_varlen_fwd(q, k, v, cu, cu, maxlen, True, scale, out, lse, ws_f)
+    B.bs_attn_varlen_bwd(q, k, v, out, lse, do, cu, cu, maxlen, True, scale, dq, dk, dv, ws_b)
+
+
+def _event_ms(fn, dev, reps=5, warmup=2):
+    import torch
+    for _ in range(warmup):
+        fn()
+    s = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    for _ in range(reps):
+        fn()
+    e1.record(s)
+    torch.cuda.synchronize(dev)
+    return e0.elapsed_time(e1) / reps
+
+
+def _host_link_gbs(dev):
+    """B_d2h and B_h2d (Sec. 4 profiles them): 1 GiB copies between pinned host memory and HBM."""
+    import torch
+    n = 1 << 30
+    h = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    g = torch.empty(n, dtype=torch.uint8, device=dev)
+    h2d = _event_ms(lambda: g.copy_(h, non_blocking=True), dev, reps=3, warmup=1)
+    d2h = _event_ms(lambda: h.copy_(g, non_blocking=True), dev, reps=3, warmup=1)
+    return n / (d2h * 1e-3), n / (h2d * 1e-3)
+
+
+def _replay(mbs, unit_ms, d):
+    """Finish time of every rank when the plan's units take unit_ms[k] (a unit's ranks start it
+    together when the last of them is free)."""
+    fin = [0.0] * d
+    for k, (_, ranks, _, _, _) in enumerate(mbs):
+        start = max(fin[g] for g in ranks)
+        for g in ranks:
+            fin[g] = start + unit_ms[k]
+    return fin
+
+
+def run_hdp_bench(args, dev):
+    """Plans a long-tailed global batch with the native planners, using a cost model fitted from
+    this library's own attention times, then runs every micro-batch on the GPU: the modelled
+    per-rank finish times of the naive and balanced plans are set against the measured ones."""
+    import numpy as np
+    import torch
+    from paper_2502_21231_amd import bs_attn as B
+    from paper_2502_21231_amd import hdp as N
+    from paper_2502_21231_amd import inputs
+    cfg = HDP
+    hq, hkv, d = cfg["hq"], cfg["hkv"], cfg["d"]
+    C, R = cfg["capacity"], cfg["ranks"]
+    scale = 1.0 / math.sqrt(d)
+    lens = inputs.lognormal_packed_lengths(args.seed, cfg["total"], hi=cfg["max_len"])
+    T = sum(lens)
+    q = inputs.normal(args.seed, inputs.TID_Q, (T, hq, d)).to(dev)
+    k = inputs.normal(args.seed, inputs.TID_K, (T, hkv, d)).to(dev)
+    v = inputs.normal(args.seed, inputs.TID_V, (T, hkv, d)).to(dev)
+    do = inputs.normal(args.seed, inputs.TID_DO, (T, hq, d)).to(dev)
+    starts = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+
+    # 1. T(s) of this library: attention fwd+bwd of one sequence, least squares over lengths
+    fit_ms = []
+    for L in cfg["fit_lengths"]:
+        sl = slice(0, L)
+        qs, ks, vs, dos = (t[sl].contiguous() for t in (q, k, v, do))
+        cu = torch.tensor([0, L], dtype=torch.int32, device=dev)
+        dims = B.make_dims(qs, ks)
+        wf = B.alloc_workspace(B.BS_OP_VARLEN_FWD, dims, dev, 1, L)
+        wb = B.alloc_workspace(B.BS_OP_VARLEN_BWD, dims, dev, 1, L)
+        bufs = (torch.empty_like(qs), torch.empty(hq, L, device=dev), torch.empty_like(qs),
+                torch.empty_like(ks), torch.empty_like(vs))
+        fit_ms.append(_event_ms(lambda: _varlen_call(qs, ks, vs, dos, cu, L, wf, wb, *bufs, scale), dev))
+    # non-negative least squares on relative errors (each length weighs alike)
+    from scipy.optimize import nnls
+    Ls = np.array(cfg["fit_lengths"], dtype=np.float64)
+    y = np.array(fit_ms) * 1e-3
+    A = np.stack([Ls * Ls, Ls, np.ones_like(Ls)], axis=1) / y[:, None]
+    coef, _ = nnls(A, np.ones_like(y))
+    a1, b1, g0 = (float(x) for x in coef)
+    bw_d2h, bw_h2d = _host_link_gbs(dev)
+    cost = N.make_cost(a1, b1, g0, float(cfg["act_bytes_per_token"]), 0.0, cfg["layers"], bw_d2h, bw_h2d)
+
+    # 2. the plans (native planners; the oracle planners timed on the same batch for reference)
+    plans, plan_ms = {}, {}
+    for name, alg in (("naive", N.NAIVE), ("dp_balance", N.DP_BALANCE), ("pp_balance", N.PP_BALANCE)):
+        t0 = time.perf_counter()
+        plans[name] = N.plan(alg, lens, C, R, cost, cfg["delta"], cfg["buckets"])
+        plan_ms[name] = (time.perf_counter() - t0) * 1e3
+
+    # 3. every unit's measured time: a packed micro-batch runs as one varlen call; a
+    # context-parallel sequence runs once, whole, and each of its D ranks is charged 1/D of it
+    # (the zig-zag split gives every rank of the group the same mask area)
+    unit_cache = {}
+
+    def unit(seqs):
+        key = tuple(sorted(seqs))
+        if key in unit_cache:
+            return unit_cache[key]
+        rows = np.concatenate([np.arange(starts[i], starts[i + 1]) for i in key])
+        ri = torch.from_numpy(rows).to(dev)
+        qs, ks, vs, dos = (t.index_select(0, ri) for t in (q, k, v, do))
+        seg = [lens[i] for i in key]
+        cu = torch.from_numpy(inputs.cu_seqlens(seg)).to(dev)
+        dims = B.make_dims(qs, ks)
+        ml = max(seg)
+        wf = B.alloc_workspace(B.BS_OP_VARLEN_FWD, dims, dev, len(seg), ml)
+        wb = B.alloc_workspace(B.BS_OP_VARLEN_BWD, dims, dev, len(seg), ml)
+        bufs = (torch.empty_like(qs), torch.empty(hq, qs.shape[0], device=dev), torch.empty_like(qs),
+                torch.empty_like(ks), torch.empty_like(vs))
+        fn = (lambda: _varlen_call(qs, ks, vs, dos, cu, ml, wf, wb, *bufs, scale))
+        unit_cache[key] = (fn, seg)
+        return unit_cache[key]
+
+    hdp_report = {"cost_fit": {"alpha1_s_per_token2": a1, "beta1_s_per_token": b1, "gamma_s": g0,
+                               "lengths": cfg["fit_lengths"], "measured_ms": fit_ms,
+                               "model_ms": [float((a1 * L * L + b1 * L + g0) * 1e3) for L in cfg["fit_lengths"]]},
+                  "bw_d2h_gbs": bw_d2h / 1e9, "bw_h2d_gbs": bw_h2d / 1e9,
+                  "act_bytes_per_token_per_layer": cfg["act_bytes_per_token"], "layers": cfg["layers"],
+                  "sequences": len(lens), "longest": max(lens),
+                  "long_sequences": sum(1 for L in lens if L > C), "plans": {}}
+    for name, (mbs, rank_time) in plans.items():
+        unit_ms = []
+        for seqs, ranks, r, start, t in mbs:
+            fn, seg = unit(seqs)
+            unit_ms.append(_event_ms(fn, dev, reps=3, warmup=1) / len(ranks))
+        fin = _replay(mbs, unit_ms, R)
+        bub = lambda f: 1.0 - sum(f) / (len(f) * max(f))
+        hdp_report["plans"][name] = {
+            "micro_batches": len(mbs), "plan_ms_native": plan_ms[name],
+            "model_makespan_ms": max(rank_time) * 1e3, "model_bubble": bub(rank_time),
+            "measured_makespan_ms": max(fin), "measured_bubble": bub(fin),
+            "measured_rank_ms": fin, "model_rank_ms": [x * 1e3 for x in rank_time],
+            "offloaded": [[list(s), r] for s, _, r, _, _ in mbs if r > 0]}
+    from oracle import hdp as H
+    oc = H.Cost(a1, b1, g0, float(cfg["act_bytes_per_token"]), 0.0, cfg["layers"], bw_d2h, bw_h2d)
+    t0 = time.perf_counter()
+    H.plan(H.ALG_DP_BALANCE, lens, C, R, oc, cfg["delta"], cfg["buckets"])
+    hdp_report["plan_ms_oracle_dp_balance"] = (time.perf_counter() - t0) * 1e3
+    # the native planners at cluster scale: 32M tokens (about 30K sequences) on 1024 ranks of 32K
+    big = inputs.lognormal_packed_lengths(args.seed, 1 << 25, hi=1 << 20)
+    scale_ms = {}
+    for name, alg in (("naive", N.NAIVE), ("dp_balance", N.DP_BALANCE), ("pp_balance", N.PP_BALANCE)):
+        t0 = time.perf_counter()
+        N.plan(alg, big, 32768, 1024, cost, cfg["delta"], 16)
+        scale_ms[name] = (time.perf_counter() - t0) * 1e3
+    hdp_report["native_plan_ms_32m_tokens_1024_ranks"] = {"sequences": len(big), **scale_ms}
+
+    # 4. the timed step: every micro-batch of the DP-Balance plan, a CP sequence once
+    mbs = plans["dp_balance"][0]
+    fns = [unit(seqs)[0] for seqs, *_ in mbs]
+
+    def step():
+        for fn in fns:
+            fn()
+
+    A_pairs = sum(L * (L + 1) // 2 for L in lens)
+    res = time_steps(step, args, dev, 4 * d * hq * A_pairs, 10 * d * hq * A_pairs)
+    res["config"] = {"workload": WORKLOADS[args.workload], "tokens": T, "heads_q": hq, "heads_kv": hkv,
+                     "head_dim": d, "capacity": C, "ranks": R, "seed": args.seed,
+                     "visible_pairs": A_pairs}
+    res["flops_per_step"] = 14 * d * hq * A_pairs
+    res["hdp"] = hdp_report
+    return res
 
 
 def run_xent_bench(args, dev):
@@ -568,6 +745,8 @@ def main():
         res = run_zigzag_packed_bench(args, dev)
     elif args.workload == "cp7b_ring":
         res = run_cp_ring_bench(args, dev)
+    elif args.workload == "hdp_batch7b":
+        res = run_hdp_bench(args, dev)
     elif args.workload == "xent_llama3_256k":
         res = run_xent_bench(args, dev)
         line = {"metric": res["metric"], "value": round(res["value"], 3), "unit": res["unit"], "n_gpus": 1,
@@ -596,6 +775,7 @@ def main():
         "roofline": res["roofline"],
         "lse_merge_gbs": res.get("lse_merge_gbs"),
         "ring_copies": res.get("ring_copies"),
+        "hdp": res.get("hdp"),
         "cpu_baseline": res.get("cpu_baseline"),
     }
     print(json.dumps(line), flush=True)

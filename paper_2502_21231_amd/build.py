@@ -1,10 +1,11 @@
-"""Builds libbs_attn.so (HIP for gfx950) in-tree with hipcc.
+"""Builds libbs_attn.so (HIP for gfx950) in-tree with hipcc, and libbs_hdp.so (host-only
+planners) with the host C++ compiler.
 
     python -m paper_2502_21231_amd.build [-v]
 
 Every source is compiled on every call (the build check must really compile);
-objects go to paper_2502_21231_amd/_build/, the library to
-paper_2502_21231_amd/libbs_attn.so.
+objects go to paper_2502_21231_amd/_build/, the libraries to
+paper_2502_21231_amd/libbs_attn.so and paper_2502_21231_amd/libbs_hdp.so.
 """
 from __future__ import annotations
 
@@ -20,6 +21,10 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libbs_attn.so")
 
 SOURCES = ["plan.hip", "fwd_bf16.hip", "bwd_bf16.hip", "f32.hip", "rowwise.hip", "xent.hip", "capi.hip"]
+# host-only planners (no GPU code): a library of their own, built with the host compiler
+HDP_SOURCE = "hdp.cpp"
+HDP_LIB = os.path.join(PKG, "libbs_hdp.so")
+HDP_CFLAGS = ["-O2", "-std=c++17", "-fPIC", "-shared", "-ffp-contract=off", "-Wall", "-Wextra"]
 
 ARCH = "gfx950"
 CFLAGS = [
@@ -51,8 +56,25 @@ def _run(cmd, verbose):
         print(out, flush=True)
 
 
+def host_cxx() -> str:
+    for cand in (shutil.which("g++"), shutil.which("c++"), shutil.which("clang++")):
+        if cand:
+            return cand
+    raise RuntimeError("no host C++ compiler found (g++) to build libbs_hdp.so")
+
+
+def build_hdp(verbose: bool = False) -> str:
+    """Compiles the host planners into libbs_hdp.so; returns its path."""
+    tmp = HDP_LIB + ".tmp"
+    _run([host_cxx(), *HDP_CFLAGS, os.path.join(CSRC, HDP_SOURCE), "-o", tmp], verbose)
+    os.replace(tmp, HDP_LIB)
+    return HDP_LIB
+
+
 def build(verbose: bool = False, jobs: int | None = None) -> str:
-    """Compiles all HIP sources for gfx950 and links libbs_attn.so; returns its path."""
+    """Compiles all HIP sources for gfx950 and links libbs_attn.so, and builds the host planners'
+    libbs_hdp.so; returns the path of libbs_attn.so."""
+    build_hdp(verbose)
     cc = hipcc()
     os.makedirs(BUILD, exist_ok=True)
     objs = []

@@ -1,0 +1,127 @@
+"""Parity of the native HDP planners (libbs_hdp.so, C ABI of include/bs_hdp.h) with the oracle:
+every decision bit for bit (micro-batch membership and order, ranks, offload ratios, modelled
+start and duration, every rank's finish time) on seeded batches, plus the C ABI's error paths.
+Host code only: these run without a GPU."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import hdp as H
+from paper_2502_21231_amd import hdp as N
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+K = 1024
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(N.LIB_PATH):
+        pytest.fail("libbs_hdp.so is not built (run __graft_entry__.build())")
+    return N.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "bs_hdp.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(bs_hdp_\w+)\s*\(", text)))
+    assert set(names) == set(N.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def random_cost(rng):
+    return H.Cost(float(rng.choice([0.0, rng.uniform(1e-12, 5e-11)])), float(rng.uniform(0, 1e-7)),
+                  float(rng.uniform(0, 1e-4)), float(rng.uniform(1e4, 1e6)),
+                  float(rng.choice([0.0, rng.uniform(0, 1e8)])), int(rng.integers(3, 81)),
+                  float(rng.choice([0.0, rng.uniform(1e9, 1e11)])), float(rng.uniform(1e9, 1e11)))
+
+
+def random_batch(rng, C, d, cost):
+    """Log-normal lengths (a long tail past the capacity), a few exact repeats and boundary
+    lengths (C, C + 1, 1), keeping every long sequence within d ranks."""
+    n = int(rng.integers(0, 600))
+    med = float(rng.uniform(256, 8192))
+    lens = [int(max(1, x)) for x in rng.lognormal(math.log(med), float(rng.uniform(0.5, 2.0)), n)]
+    lens += [C, C + 1, 1, lens[0] if lens else 7, lens[0] if lens else 7]
+    out = []
+    for s in lens:
+        while s > C and H.offload_ratio(s, C, cost)[1] > d:
+            s = s // 2
+        out.append(max(1, s))
+    return out
+
+
+@pytest.mark.parametrize("alg", [H.ALG_NAIVE, H.ALG_DP_BALANCE, H.ALG_PP_BALANCE])
+def test_native_plans_equal_the_oracle_bit_for_bit(lib, alg):
+    rng = np.random.default_rng(2025 + alg)
+    for trial in range(60):
+        cost = random_cost(rng)
+        C = int(rng.choice([1024, 4096, 8192, 32768, 65536]))
+        d = int(rng.integers(1, 65))
+        delta = float(rng.choice([0.0, rng.uniform(0, 1e-2)]))
+        nb = int(rng.integers(1, 12))
+        lens = random_batch(rng, C, d, cost)
+        want = H.plan(alg, lens, C, d, cost, delta, nb)
+        got = N.plan(alg, lens, C, d, cost, delta, nb)
+        assert got[0] == want[0], (trial, alg)
+        assert got[1] == want[1], (trial, alg)
+
+
+def test_eq3_equals_the_oracle_bit_for_bit(lib):
+    rng = np.random.default_rng(7)
+    for _ in range(2000):
+        cost = random_cost(rng)
+        C = int(rng.integers(1, 1 << 17))
+        s = int(rng.integers(1, 1 << 24))
+        assert N.offload_ratio(s, C, cost) == H.offload_ratio(s, C, cost)
+
+
+def test_edge_batches(lib):
+    cost = H.Cost(1e-11, 1e-8, 1e-6, 1e5, 0.0, 32, 5e10, 5e10)
+    for alg in (H.ALG_NAIVE, H.ALG_DP_BALANCE, H.ALG_PP_BALANCE):
+        for lens, C, d, nb in (([], 4096, 4, 3),                     # empty batch
+                               ([4096] * 10, 4096, 4, 3),            # every sequence exactly C
+                               ([1] * 500, 4096, 1, 1),              # one rank, one bucket
+                               ([5000, 9000, 20000], 4096, 8, 16),   # only long ones, more buckets than sequences
+                               ([100, 200, 300], 4096, 64, 2)):      # more ranks than work
+            assert N.plan(alg, lens, C, d, cost, 1e-4, nb) == H.plan(alg, lens, C, d, cost, 1e-4, nb)
+
+
+def test_error_paths(lib):
+    cost = N.make_cost(1e-11, 1e-8, 1e-6, 1e5, 0.0, 32, 0.0, 0.0)
+    with pytest.raises(N.HdpError) as e:
+        N.plan(N.NAIVE, [64 * K], 1024, 4, cost)  # needs 64 ranks without offloading
+    assert e.value.status == N.BS_HDP_ERR_INFEASIBLE
+    with pytest.raises(N.HdpError) as e:
+        N.plan(N.DP_BALANCE, [64 * K], 1024, 4, cost)
+    assert e.value.status == N.BS_HDP_ERR_INFEASIBLE
+    bad = N.make_cost(1e-11, 1e-8, 1e-6, 1e5, 0.0, 2, 0.0, 0.0)  # layers < 3
+    with pytest.raises(N.HdpError) as e:
+        N.plan(N.NAIVE, [10], 1024, 4, bad)
+    assert e.value.status == N.BS_HDP_ERR_INVALID_ARG and "layers" in str(e.value)
+    for fields in ((-1.0, 0.0, 0.0, 1e5, 0.0), (0.0, 0.0, 0.0, 0.0, 0.0), (float("nan"), 0, 0, 1e5, 0)):
+        with pytest.raises(N.HdpError):
+            N.offload_ratio(10, 4, N.make_cost(*fields, 32, 0.0, 0.0))
+    with pytest.raises(N.HdpError):
+        N.plan(N.NAIVE, [0, 5], 1024, 4, cost)  # a sequence of zero tokens
+    with pytest.raises(N.HdpError):
+        N.plan(7, [5], 1024, 4, cost)  # unknown algorithm
+    with pytest.raises(N.HdpError):
+        N.plan(N.DP_BALANCE, [5], 1024, 4, cost, delta=-1.0)
+    # output arrays too small: a plan of 3 micro-batches into room for 1
+    lens = np.array([800, 800, 800], dtype=np.int64)
+    mbs = (N.bs_hdp_microbatch * 1)()
+    seqs = np.empty(3, np.int32)
+    ranks = np.empty(3, np.int32)
+    rt = np.empty(2, np.float64)
+    n = ctypes.c_int32(-5)
+    c = cost
+    rc = lib.bs_hdp_plan(N.NAIVE, ctypes.byref(c), lens.ctypes.data, 3, 1024, 2, 0.0, 1,
+                         ctypes.cast(mbs, ctypes.c_void_p), 1, seqs.ctypes.data, ranks.ctypes.data, 3,
+                         ctypes.byref(n), rt.ctypes.data)
+    assert rc == N.BS_HDP_ERR_CAPACITY and n.value == -5  # nothing written
+    assert lib.bs_hdp_plan(N.NAIVE, None, None, 0, 1, 1, 0.0, 1, None, 0, None, None, 0,
+                           ctypes.byref(n), rt.ctypes.data) == N.BS_HDP_ERR_INVALID_ARG

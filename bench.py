@@ -5,9 +5,12 @@
 A step is one causal attention forward + backward of the workload through the
 C ABI: device planning, forward, backward preprocess, backward, dQ finalize
 (and for the context-parallel workloads the per-step chunk calls plus the LSE
-merge).  Inputs are resident in HBM before timing starts; K steps are timed
-with HIP events on the library's stream, bracketed by device synchronisation.
-Prints ONE JSON line.
+merge, or the running merge of the ring rehearsal).  Two workloads measure the
+other rows of the build: hdp_batch7b (the HDP planners, checked by running every
+planned micro-batch) and xent_llama3_256k (the fused softmax cross-entropy, its
+own HBM metric).  Inputs are resident in HBM before timing starts; K steps are
+timed with HIP events on the library's stream, bracketed by device
+synchronisation.  Prints ONE JSON line.
 
 FLOPs are causal-adjusted: forward 4*d*Hq*A, backward 10*d*Hq*A, where A is
 the exact number of visible (query, key) pairs.

@@ -125,3 +125,15 @@ def test_error_paths(lib):
     assert rc == N.BS_HDP_ERR_CAPACITY and n.value == -5  # nothing written
     assert lib.bs_hdp_plan(N.NAIVE, None, None, 0, 1, 1, 0.0, 1, None, 0, None, None, 0,
                            ctypes.byref(n), rt.ctypes.data) == N.BS_HDP_ERR_INVALID_ARG
+
+
+def test_benchmark_batch_plans_equal_the_oracle(lib):
+    """The global batch and cost model of the planner benchmark (524288 tokens, 16 ranks of 8K,
+    T(s) of the measured attention, 57 GB/s host links): every algorithm's plan bit for bit."""
+    from paper_2502_21231_amd import inputs
+    lens = inputs.lognormal_packed_lengths(0, 524288, hi=131072)
+    cost = H.Cost(3.38e-11, 2.37e-8, 7.6e-5, 34 * 4096, 0.0, 32, 57e9, 57.3e9)
+    for alg in (H.ALG_NAIVE, H.ALG_DP_BALANCE, H.ALG_PP_BALANCE):
+        want = H.plan(alg, lens, 8192, 16, cost, 1e-4, 4)
+        assert N.plan(alg, lens, 8192, 16, cost, 1e-4, 4) == want
+        assert any(r > 0 for _, _, r, _, _ in want[0])  # Eq. 3 offloads some of its sequences

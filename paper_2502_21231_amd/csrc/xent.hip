@@ -5,11 +5,12 @@
 //
 // Bandwidth-bound, one workgroup per row, in two forms.  bf16 rows of 16K..128K entries (the
 // vocabularies of current LLMs up to LLaMA3's) use the register-resident form below: the row is read from HBM
-// once into registers and its gradient written from there.  Other rows are streamed twice.
-// Streaming form: pass 1 streams the row with 16-byte loads and keeps
+// once into registers and its gradient written from there.  Other rows are streamed twice by a
+// persistent grid that keeps one row per CU in flight, so that the second pass finds the row in
+// the caches.  Streaming form: pass 1 streams the row with 16-byte loads and keeps
 // a running (max, sum of 2^(x - max)) per lane in the log2 domain; the max is raised only when a
 // chunk exceeds it by 2^8, so the sum is rescaled almost never and its terms stay below 2^8.
-// The lanes' pairs are combined in a fixed order (wave shuffles, then the 4 waves through LDS),
+// The lanes' pairs are combined in a fixed order (wave shuffles, then the waves through LDS),
 // so every run gives the same bits.  Pass 2 reads the row again (it is still in the XCD's L2 or
 // the last-level cache: the same workgroup read it microseconds before), forms
 // g * (2^(x - lse) - [j == label]) and writes it.  HBM traffic per element: the logit read once
@@ -19,7 +20,7 @@
 namespace bs {
 namespace {
 
-constexpr int kXentThreads = 256;
+constexpr int kXentThreads = 1024;
 constexpr float kXentRescale = 8.0f;  // log2 units
 
 struct XentParams {
@@ -91,93 +92,100 @@ __device__ __forceinline__ void store_f(T* dst, const float (&g)[N]) {
 }
 
 // VEC: 16-byte chunks (vocab a multiple of the vector width, rows 16-byte aligned); otherwise
-// one element per lane and step.
+// one element per lane and step.  Persistent: one workgroup of kXentThreads lanes per CU walks
+// the rows strided by the grid, so that only one row per CU is in flight and the second pass
+// finds it in the caches (a row is read from HBM once as long as the rows in flight, CUs x row
+// bytes, fit the last-level cache).
 template <typename T, bool VEC>
-__global__ __launch_bounds__(kXentThreads) void xent_kernel(const XentParams p) {
+__global__ __launch_bounds__(kXentThreads) void xent_kernel(const XentParams p, int64_t rows) {
   constexpr int N = VEC ? XVec<T>::N : 1;
   constexpr int U = VEC ? 4 : 8;  // chunks in flight per lane
-  const int64_t row = blockIdx.x;
+  constexpr int NW = kXentThreads / 64;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const T* zr = static_cast<const T*>(p.logits) + row * p.vocab;
-  const int64_t y = p.labels[row];
-  const bool ignored = y == p.ignore_index;
-  const bool in_range = y >= 0 && y < p.vocab;
   const int64_t nch = p.vocab / N;
+  __shared__ float red_m[2][NW], red_s[2][NW];
+  int it = 0;
+  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x, ++it) {
+    const T* zr = static_cast<const T*>(p.logits) + row * p.vocab;
+    const int64_t y = p.labels[row];
+    const bool ignored = y == p.ignore_index;
+    const bool in_range = y >= 0 && y < p.vocab;
 
-  // pass 1: running (max, sum) per lane
-  float m = -INFINITY, s = 0.f;
-  int64_t c = tid;
-  for (; c + (U - 1) * kXentThreads < nch; c += U * kXentThreads) {
-    float z[U][N];
+    // pass 1: running (max, sum) per lane
+    float m = -INFINITY, s = 0.f;
+    int64_t c = tid;
+    for (; c + (U - 1) * kXentThreads < nch; c += U * kXentThreads) {
+      float z[U][N];
 #pragma unroll
-    for (int u = 0; u < U; ++u) load_f<T, N>(zr + (c + u * kXentThreads) * N, z[u]);
+      for (int u = 0; u < U; ++u) load_f<T, N>(zr + (c + u * kXentThreads) * N, z[u]);
 #pragma unroll
-    for (int u = 0; u < U; ++u) accumulate<N>(z[u], m, s);
-  }
-  for (; c < nch; c += kXentThreads) {
-    float z[N];
-    load_f<T, N>(zr + c * N, z);
-    accumulate<N>(z, m, s);
-  }
-  // the label's logit, read before any gradient can overwrite it (in-place use)
-  float zy = 0.f;
-  if (tid == 0 && !ignored && in_range) zy = (float)zr[y];
-
-  // fixed-order reduction: within the wave, then the 4 waves
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const float m2 = __shfl_xor(m, off), s2 = __shfl_xor(s, off);
-    combine(m, s, m2, s2);
-  }
-  __shared__ float red_m[kXentThreads / 64], red_s[kXentThreads / 64];
-  if (lane == 0) {
-    red_m[w] = m;
-    red_s[w] = s;
-  }
-  __syncthreads();
-  m = red_m[0];
-  s = red_s[0];
-#pragma unroll
-  for (int i = 1; i < kXentThreads / 64; ++i) combine(m, s, red_m[i], red_s[i]);
-  const float lse2 = m == -INFINITY ? -INFINITY : m + log2f(s);
-  if (tid == 0) {
-    if (p.lse != nullptr) p.lse[row] = lse2 * kLn2;
-    p.loss[row] = ignored ? 0.f : (in_range ? lse2 * kLn2 - zy : NAN);
-  }
-  if (p.dlogits == nullptr) return;
-
-  // pass 2: gradient g (2^(x - lse2) - [j == label]); an ignored row is written as zeros
-  T* dr = static_cast<T*>(p.dlogits) + row * p.vocab;
-  const float g = p.grad_scale;
-  const int64_t cy = in_range && !ignored ? y / N : -1;
-  const int ky = (int)(y - cy * N);
-  auto grad = [&](int64_t cc, const float (&z)[N]) {
-    float o[N];
-#pragma unroll
-    for (int k = 0; k < N; ++k) o[k] = fast_exp2(fmaf(z[k], kLog2e, -lse2)) * g;
-    if (cc == cy) {
-#pragma unroll
-      for (int k = 0; k < N; ++k) o[k] = k == ky ? o[k] - g : o[k];
+      for (int u = 0; u < U; ++u) accumulate<N>(z[u], m, s);
     }
-    store_f<T, N>(dr + cc * N, o);
-  };
-  c = tid;
-  if (ignored) {
-    const float zero[N] = {};
-    for (; c < nch; c += kXentThreads) store_f<T, N>(dr + c * N, zero);
-    return;
-  }
-  for (; c + (U - 1) * kXentThreads < nch; c += U * kXentThreads) {
-    float z[U][N];
+    for (; c < nch; c += kXentThreads) {
+      float z[N];
+      load_f<T, N>(zr + c * N, z);
+      accumulate<N>(z, m, s);
+    }
+    // the label's logit, read before any gradient can overwrite it (in-place use)
+    float zy = 0.f;
+    if (tid == 0 && !ignored && in_range) zy = (float)zr[y];
+
+    // fixed-order reduction: within the wave, then the waves (two buffers, alternating by row)
 #pragma unroll
-    for (int u = 0; u < U; ++u) load_f<T, N>(zr + (c + u * kXentThreads) * N, z[u]);
+    for (int off = 32; off > 0; off >>= 1) {
+      const float m2 = __shfl_xor(m, off), s2 = __shfl_xor(s, off);
+      combine(m, s, m2, s2);
+    }
+    const int rb = it & 1;
+    if (lane == 0) {
+      red_m[rb][w] = m;
+      red_s[rb][w] = s;
+    }
+    __syncthreads();
+    m = red_m[rb][0];
+    s = red_s[rb][0];
 #pragma unroll
-    for (int u = 0; u < U; ++u) grad(c + u * kXentThreads, z[u]);
-  }
-  for (; c < nch; c += kXentThreads) {
-    float z[N];
-    load_f<T, N>(zr + c * N, z);
-    grad(c, z);
+    for (int i = 1; i < NW; ++i) combine(m, s, red_m[rb][i], red_s[rb][i]);
+    const float lse2 = m == -INFINITY ? -INFINITY : m + log2f(s);
+    if (tid == 0) {
+      if (p.lse != nullptr) p.lse[row] = lse2 * kLn2;
+      p.loss[row] = ignored ? 0.f : (in_range ? lse2 * kLn2 - zy : NAN);
+    }
+    if (p.dlogits == nullptr) continue;
+
+    // pass 2: gradient g (2^(x - lse2) - [j == label]); an ignored row is written as zeros
+    T* dr = static_cast<T*>(p.dlogits) + row * p.vocab;
+    const float g = p.grad_scale;
+    const int64_t cy = in_range && !ignored ? y / N : -1;
+    const int ky = (int)(y - cy * N);
+    auto grad = [&](int64_t cc, const float (&z)[N]) {
+      float o[N];
+#pragma unroll
+      for (int k = 0; k < N; ++k) o[k] = fast_exp2(fmaf(z[k], kLog2e, -lse2)) * g;
+      if (cc == cy) {
+#pragma unroll
+        for (int k = 0; k < N; ++k) o[k] = k == ky ? o[k] - g : o[k];
+      }
+      store_f<T, N>(dr + cc * N, o);
+    };
+    c = tid;
+    if (ignored) {
+      const float zero[N] = {};
+      for (; c < nch; c += kXentThreads) store_f<T, N>(dr + c * N, zero);
+      continue;
+    }
+    for (; c + (U - 1) * kXentThreads < nch; c += U * kXentThreads) {
+      float z[U][N];
+#pragma unroll
+      for (int u = 0; u < U; ++u) load_f<T, N>(zr + (c + u * kXentThreads) * N, z[u]);
+#pragma unroll
+      for (int u = 0; u < U; ++u) grad(c + u * kXentThreads, z[u]);
+    }
+    for (; c < nch; c += kXentThreads) {
+      float z[N];
+      load_f<T, N>(zr + c * N, z);
+      grad(c, z);
+    }
   }
 }
 
@@ -312,27 +320,27 @@ hipError_t launch_softmax_xent(int64_t rows, int64_t vocab, int dtype, const voi
   const bool aligned = reinterpret_cast<uintptr_t>(logits) % 16 == 0 &&
                        (dlogits == nullptr || reinterpret_cast<uintptr_t>(dlogits) % 16 == 0);
   const bool vec = aligned && vocab % vw == 0;
-  const dim3 grid((unsigned)rows), block(kXentThreads);
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess)
+    hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  const dim3 grid((unsigned)(rows < cus ? rows : cus));  // persistent: one workgroup per CU
+  const dim3 block(kXentThreads);
   // bf16 rows of 16K..128K entries: the register-resident form (one HBM read per element; 24
   // chunks per lane would spill under the 1024-lane register budget)
   if (dtype == BS_BF16 && vec && vocab > 16384 && vocab <= 8 * kXentRegThreads * 16) {
     const dim3 rblock(kXentRegThreads);
     const int64_t per = (vocab / 8 + kXentRegThreads - 1) / kXentRegThreads;  // chunks per lane
-    int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) == hipSuccess)
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    const dim3 rgrid((unsigned)(rows < cus ? rows : cus));  // one resident workgroup per CU
-    if (per <= 4) hipLaunchKernelGGL(xent_reg_kernel<4>, rgrid, rblock, 0, stream, p, rows);
-    else if (per <= 8) hipLaunchKernelGGL(xent_reg_kernel<8>, rgrid, rblock, 0, stream, p, rows);
-    else hipLaunchKernelGGL(xent_reg_kernel<16>, rgrid, rblock, 0, stream, p, rows);
+    if (per <= 4) hipLaunchKernelGGL(xent_reg_kernel<4>, grid, rblock, 0, stream, p, rows);
+    else if (per <= 8) hipLaunchKernelGGL(xent_reg_kernel<8>, grid, rblock, 0, stream, p, rows);
+    else hipLaunchKernelGGL(xent_reg_kernel<16>, grid, rblock, 0, stream, p, rows);
     return hipGetLastError();
   }
   if (dtype == BS_BF16) {
-    if (vec) hipLaunchKernelGGL((xent_kernel<bf16, true>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((xent_kernel<bf16, false>), grid, block, 0, stream, p);
+    if (vec) hipLaunchKernelGGL((xent_kernel<bf16, true>), grid, block, 0, stream, p, rows);
+    else hipLaunchKernelGGL((xent_kernel<bf16, false>), grid, block, 0, stream, p, rows);
   } else {
-    if (vec) hipLaunchKernelGGL((xent_kernel<float, true>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((xent_kernel<float, false>), grid, block, 0, stream, p);
+    if (vec) hipLaunchKernelGGL((xent_kernel<float, true>), grid, block, 0, stream, p, rows);
+    else hipLaunchKernelGGL((xent_kernel<float, false>), grid, block, 0, stream, p, rows);
   }
   return hipGetLastError();
 }

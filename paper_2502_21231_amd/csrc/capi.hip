@@ -524,6 +524,11 @@ int bs_softmax_xent(int64_t rows, int64_t vocab, int dtype, const void* logits,
   if (reinterpret_cast<uintptr_t>(logits) % esize != 0 ||
       (dlogits != nullptr && reinterpret_cast<uintptr_t>(dlogits) % esize != 0))
     return fail(BS_ERR_INVALID_ARG, "logits / dlogits not aligned to their element size");
+  if (reinterpret_cast<uintptr_t>(labels) % 8 != 0 || reinterpret_cast<uintptr_t>(loss) % 4 != 0 ||
+      (lse != nullptr && reinterpret_cast<uintptr_t>(lse) % 4 != 0))
+    return fail(BS_ERR_INVALID_ARG, "labels / loss / lse not aligned to their element size");
+  if (rows > INT64_MAX / esize / vocab)
+    return fail(BS_ERR_INVALID_ARG, "rows * vocab elements exceed the address range");
   const int64_t nbytes = rows * vocab * esize;
   if (dlogits != nullptr && dlogits != logits && overlaps(dlogits, nbytes, logits, nbytes))
     return fail(BS_ERR_INVALID_ARG, "dlogits overlaps logits without being equal to it");

@@ -96,6 +96,8 @@ def test_softmax_xent_rejects_bad_arguments(lib):
     assert xent(loss=None) == B.BS_ERR_INVALID_ARG
     assert xent(logits=FAKE + 1) == B.BS_ERR_INVALID_ARG  # bf16 needs 2-byte alignment
     assert "aligned" in B.bs_last_error()
+    assert xent(labels=FAKE + 4) == B.BS_ERR_INVALID_ARG  # int64 labels need 8-byte alignment
+    assert xent(loss=FAKE + 2) == B.BS_ERR_INVALID_ARG
     # a gradient buffer that overlaps the logits without being them
     assert xent(dlogits=FAKE + 64) == B.BS_ERR_INVALID_ARG
     assert "overlaps" in B.bs_last_error()

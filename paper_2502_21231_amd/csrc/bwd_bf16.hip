@@ -141,8 +141,9 @@ void dq_bf16_kernel(const BwdParams p) {
   __syncthreads();
 
   auto step = [&](int t, const bf16* Kb, const bf16* Vb, bf16* Kn, bf16* Vn) {
-    if (t + 1 < n_tiles) copy_tile(t + 1, Kn, Vn);
-    __builtin_amdgcn_sched_barrier(0);  // issue the copy before the reads below
+    // copy of tile t+1, without a branch (the last tile copies itself again into the
+    // idle buffer), one instruction after each group of score products
+    copy_tile(min(t + 1, n_tiles - 1), Kn, Vn);
 
     f32x16 sacc[2] = {f32x16{}, f32x16{}};
     f32x16 dpacc[2] = {f32x16{}, f32x16{}};
@@ -156,6 +157,11 @@ void dq_bf16_kernel(const BwdParams p) {
         const bf16x8 b = *reinterpret_cast<const bf16x8*>(&Vb[off]);
         dpacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, dof[kk], dpacc[kb], 0, 0, 0);
       }
+    }
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedVmem, 1, 0);
     }
     if (t >= n_full) {
       const int lim = lim_base - t * BN;
@@ -272,7 +278,8 @@ void dkdv_bf16_kernel(const BwdParams p) {
   const int n_iter = n_vis * p.group;
 
   // All eight waves copy query tile i (head, rows) into QDd; the first dP wave
-  // fetches its LSE rows, the second its D rows.
+  // fetches its LSE rows, the second its D rows (the other waves load a row too,
+  // unused, so that the copy has no branch and can be scheduled among the products).
   const int ct = tid - 4 * 64;  // thread index among the role-1 waves
   float row_r = 0.f;   // raw LSE / D value of one row (converted when stored)
   bool row_ok = false;  // the row lies inside the segment
@@ -285,7 +292,7 @@ void dkdv_bf16_kernel(const BwdParams p) {
     const int64_t qo = q_glob0 * qstride + (int64_t)h * D;
     dma_tile<D, BM, NW>(QDd, p.q + qo, (int)qstride, last, w, lane);
     dma_tile<D, BM, NW>(QDd + QTILE, p.dout + qo, (int)qstride, last, w, lane);
-    if (ct >= 0 && ct < 2 * BM) {
+    {
       const int r = ct & (BM - 1);
       row_ok = r <= last;
       const int64_t li = (int64_t)h * p.total_q + q_glob0 + (row_ok ? r : 0);
@@ -313,8 +320,6 @@ void dkdv_bf16_kernel(const BwdParams p) {
   // one query tile: consume (QDb, Rb) while tile i+1 is copied into (QDn, Rn),
   // which were last read one tile earlier, before the barrier that ended it
   auto step = [&](int i, const bf16* QDb, const float* Rb, bf16* QDn, float* Rn) {
-    if (i + 1 < n_iter) copy_tile(i + 1, QDn);
-    __builtin_amdgcn_sched_barrier(0);  // issue the copy before the reads below
     const int hg = i / n_vis, j = i - hg * n_vis;
     const int q_rel0 = (qt_first + j) * BM;
     const bool masked = j < n_masked;
@@ -325,6 +330,10 @@ void dkdv_bf16_kernel(const BwdParams p) {
     // (the S wave goes first on the matrix unit, so that its exponentials overlap
     // the dP wave's products)
     if (role == 0) __builtin_amdgcn_s_setprio(1);
+    // the copy of tile i+1 (the last step copies its own tile again, into the idle
+    // buffer: no branch, so the copy instructions can go among the products below
+    // instead of queueing behind one another at the top of the step)
+    copy_tile(min(i + 1, n_iter - 1), QDn);
     f32x16 s[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) s[mb] = f32x16{};
@@ -336,11 +345,13 @@ void dkdv_bf16_kernel(const BwdParams p) {
         s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, frag[kk], s[mb], 0, 0, 0);
       }
     }
-    // keep the row reads two contraction steps ahead of the products
+    // keep the row reads two contraction steps ahead of the products, with one copy
+    // instruction after each of the first product pairs
     __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * MB, 0);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       __builtin_amdgcn_sched_group_barrier(kSchedMfma, MB, 0);
+      if (kk < 6) __builtin_amdgcn_sched_group_barrier(kSchedVmem, 1, 0);
       if (kk + 2 < KK) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, MB, 0);
     }
 

@@ -81,7 +81,7 @@ __device__ __forceinline__ void barrier_lds() {
 }
 
 // Instruction classes of __builtin_amdgcn_sched_group_barrier.
-constexpr int kSchedMfma = 0x008, kSchedDsRead = 0x100;
+constexpr int kSchedMfma = 0x008, kSchedVmem = 0x010, kSchedDsRead = 0x100;
 
 // Operand of a 32x32x16 bf16 MFMA that is the TRANSPOSE of a row-major LDS tile.
 //

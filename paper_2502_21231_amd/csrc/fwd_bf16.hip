@@ -20,8 +20,11 @@
 // (buffer_load_dwordx4 ... lds, no staging registers), into row-major tiles whose
 // 16-byte chunks are XOR-swizzled so that both the row reads of K and the
 // transposing reads of V are free of bank conflicts.  Both are double-buffered:
-// the copy of tile t+1 is issued before tile t is consumed and waited for after
-// it, one barrier per key tile.  Key rows past the segment are copied from the
+// the copy of tile t+1 is issued while tile t is consumed, its instructions placed
+// one after each pair of score products (issued back to back at the top of the
+// step, every wave's copies queue behind one another), and waited for after it, one
+// barrier per key tile.  The last tile copies itself again into the idle buffer, so
+// that the copy needs no branch.  Key rows past the segment are copied from the
 // last valid row and removed by the score mask, which every ragged tile has.
 //
 // Softmax.  Scores stay raw; the scale is folded into one FMA,
@@ -129,8 +132,7 @@ void fwd_bf16_kernel(const FwdParams p) {
   // one key tile: consume (Kb, Vb) while tile t+1 is copied into (Kn, Vn), which
   // were last read one tile earlier, before the barrier that ended it
   auto step = [&](int t, const bf16* Kb, const bf16* Vb, bf16* Kn, bf16* Vn) {
-    if (t + 1 < n_tiles) copy_tile(t + 1, Kn, Vn);
-    __builtin_amdgcn_sched_barrier(0);  // issue the copy before the reads below
+    copy_tile(min(t + 1, n_tiles - 1), Kn, Vn);
 
     f32x16 sacc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
@@ -140,6 +142,11 @@ void fwd_bf16_kernel(const FwdParams p) {
         const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Kb[swz_off<D>(kb * 32 + c, kk * 2 + hh)]);
         sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], sacc[kb], 0, 0, 0);
       }
+    }
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedVmem, 1, 0);
     }
 
     // mask (MASKED tiles only): key local index kb*32 + (r/4)*8 + hh*4 + r%4

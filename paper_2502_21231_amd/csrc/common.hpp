@@ -68,6 +68,18 @@ __device__ __forceinline__ bf16 f2bf(float x) { return (bf16)x; }  // RNE on gfx
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Max / sum of this lane's value and lane (l ^ 32)'s: v_permlane32_swap exchanges the two
+// 32-lane halves of a register pair in the vector unit (a shuffle would go through LDS and
+// wait for every outstanding LDS read).  Both lanes of a pair get the same bits.
+__device__ __forceinline__ float half_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // s_waitcnt vmcnt(0) (expcnt and lgkmcnt left unconstrained): all of this
 // wave's outstanding vector-memory loads have returned.
 __device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }

@@ -163,7 +163,7 @@ void fwd_bf16_kernel(const FwdParams p) {
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
+    mx = half_max(mx) * c2;
     if (__any(mx > m2 + kRescaleThreshold)) {
       const float m_new = fmaxf(m2, mx);
       const float alpha = fast_exp2(m2 - (m_new == -INFINITY ? 0.f : m_new));
@@ -202,7 +202,7 @@ void fwd_bf16_kernel(const FwdParams p) {
     if (t + 1 < n_tiles) step(t + 1, K1, V1, K0, V0);
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = half_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   if (!qvalid) return;
   const int64_t row = it.a_start + qrow;

@@ -136,6 +136,8 @@ void dq_bf16_kernel(const BwdParams p) {
   if (p.causal) lim_base = min(k_len, q_rel + it.diag + 1);
   lim_base -= hh * 4;
 
+  // lane bases of the row reads of K and V and the transposing reads of K
+  const int rbase = swz_row_base<D>(lane), tbase = swz_tr_base<D>(lane);
   if (n_tiles > 0) copy_tile(0, K0, V0);
   wait_vmem_all();  // Q, dO fragments and tile 0
   __syncthreads();
@@ -151,17 +153,21 @@ void dq_bf16_kernel(const BwdParams p) {
     for (int kk = 0; kk < KK; ++kk) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const int off = swz_off<D>(kb * 32 + c, kk * 2 + hh);
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Kb[off]);
+        const int off = (rbase ^ (kk << 5)) + kb * 64 * D;
+        const bf16x8 a = lds_row16(Kb, off);
         sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], sacc[kb], 0, 0, 0);
-        const bf16x8 b = *reinterpret_cast<const bf16x8*>(&Vb[off]);
+        const bf16x8 b = lds_row16(Vb, off);
         dpacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, dof[kk], dpacc[kb], 0, 0, 0);
       }
     }
+    // K and V reads one contraction step ahead of the products, one copy instruction
+    // after each group of four products
+    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       __builtin_amdgcn_sched_group_barrier(kSchedMfma, 4, 0);
       __builtin_amdgcn_sched_group_barrier(kSchedVmem, 1, 0);
+      if (kk + 1 < KK) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
     }
     if (t >= n_full) {
       const int lim = lim_base - t * BN;
@@ -184,8 +190,8 @@ void dq_bf16_kernel(const BwdParams p) {
     for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const bf16x8 a = lds_read_tr2(Kb + swz_tr_off<D>(ks * 16, db * 32, 0, lane),
-                                      Kb + swz_tr_off<D>(ks * 16, db * 32, 1, lane));
+        const bf16x8 a = lds_tr16(Kb, (tbase ^ (db << 6)) + ks * 32 * D,
+                                  (tbase ^ ((db << 6) | 32)) + ks * 32 * D + 16 * D);
         dqacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[ks], dqacc[db], 0, 0, 0);
       }
     }

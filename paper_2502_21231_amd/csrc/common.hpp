@@ -157,6 +157,22 @@ __device__ __forceinline__ int swz_off(int r, int c) {
   return r * D + ((c ^ swz_g<D>(r)) << 3);
 }
 
+// The swizzle only moves bits 4..7 of a byte offset inside a row (it XORs the chunk
+// index), so a lane's reads of a tile differ by a lane-independent XOR plus a multiple of
+// a row: one lane base per access pattern gives every address with one v_xor_b32, and the
+// row part (and the tile's own LDS address) go into the instruction's immediate offset.
+//   row read of chunk (2 kk + hh) of row (32 kb + c), lane = 32 hh + c:
+//     swz_off(32 kb + c, 2 kk + hh) * 2 == (swz_row_base(lane) ^ (kk << 5)) + kb * 64 * D
+//   transposing read r of contraction rows k0 = 16 ks, columns m0 = 32 db:
+//     swz_tr_off(16 ks, 32 db, r, lane) * 2
+//         == (swz_tr_base(lane) ^ ((db << 6) | (r << 5))) + ks * 32 * D + r * 16 * D
+template <int D>
+__device__ __forceinline__ int swz_row_base(int lane) {
+  return swz_off<D>(lane & 31, lane >> 5) * 2;
+}
+template <int D>
+__device__ __forceinline__ int swz_tr_base(int lane);
+
 // One wave's share of copying rows 0..R-1 of a swizzled [R][D] bf16 tile from global
 // memory straight into LDS (buffer_load_dwordx4 ... lds: lane l of an instruction
 // writes 16 bytes at LDS base + offset + 16*l, so an instruction fills 64/(D/8) whole
@@ -216,6 +232,18 @@ __device__ __forceinline__ int swz_tr_off(int k0, int m0, int r, int lane) {
   const int row = k0 + 8 * r + 4 * (lane >> 5) + (i >> 2);
   const int col = m0 + ((lane >> 4) & 1) * 16 + (i & 3) * 4;
   return swz_off<D>(row, col >> 3) + (col & 7);
+}
+template <int D>
+__device__ __forceinline__ int swz_tr_base(int lane) {
+  return swz_tr_off<D>(0, 0, 0, lane) * 2;
+}
+// Byte-addressed LDS views used with the bases above.
+__device__ __forceinline__ bf16x8 lds_row16(const bf16* tile, int byte_off) {
+  return *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(tile) + byte_off);
+}
+__device__ __forceinline__ bf16x8 lds_tr16(const bf16* tile, int off0, int off1) {
+  const char* t = reinterpret_cast<const char*>(tile);
+  return lds_read_tr2(reinterpret_cast<const bf16*>(t + off0), reinterpret_cast<const bf16*>(t + off1));
 }
 
 }  // namespace bs

@@ -143,10 +143,14 @@ void fwd_bf16_kernel(const FwdParams p) {
         sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], sacc[kb], 0, 0, 0);
       }
     }
+    // K reads two contraction steps ahead of the products, one copy instruction after
+    // each pair of products
+    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
       __builtin_amdgcn_sched_group_barrier(kSchedVmem, 1, 0);
+      if (kk + 2 < KK) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
     }
 
     // mask (MASKED tiles only): key local index kb*32 + (r/4)*8 + hh*4 + r%4

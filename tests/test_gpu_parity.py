@@ -18,7 +18,7 @@ pytestmark = pytest.mark.gpu
 RAGGED = [1, 63, 64, 65, 127, 128, 129, 200, 3, 517]
 
 
-def run_varlen(lens, hq, hkv, d, dtype, seed=0, causal=True, bwd=True):
+def run_varlen(lens, hq, hkv, d, dtype, seed=0, causal=True, bwd=True, rel=0.0):
     T = sum(lens)
     cu = torch.from_numpy(inputs.cu_seqlens(lens))
     q, k, v, do = make_qkv(seed, T, T, hq, hkv, d, dtype)
@@ -28,7 +28,7 @@ def run_varlen(lens, hq, hkv, d, dtype, seed=0, causal=True, bwd=True):
     out, lse = B.bs_attn_varlen_fwd(qg, kg, vg, cug, cug, maxlen, causal, scale)
     o_ref, lse_ref = A.varlen_fwd(q, k, v, cu.numpy(), cu.numpy(), causal, scale)
     tol = TOL[dtype]
-    check_close("O", f64(out), o_ref, tol["o"], dtype == torch.bfloat16)
+    check_close("O", f64(out), o_ref, tol["o"], dtype == torch.bfloat16, rel)
     check_lse("LSE", f64(lse), lse_ref, tol["lse"])
     if not bwd:
         return
@@ -39,9 +39,9 @@ def run_varlen(lens, hq, hkv, d, dtype, seed=0, causal=True, bwd=True):
     dq, dk, dv = B.bs_attn_varlen_bwd(qg, kg, vg, o_in.cuda(), lse_in.cuda(), dog, cug, cug, maxlen,
                                       causal, scale)
     dq_r, dk_r, dv_r = A.varlen_bwd(q, k, v, o_in, lse_in, do, cu.numpy(), cu.numpy(), causal, scale)
-    check_close("dQ", f64(dq), dq_r, tol["grad"], dtype == torch.bfloat16)
-    check_close("dK", f64(dk), dk_r, tol["grad"], dtype == torch.bfloat16)
-    check_close("dV", f64(dv), dv_r, tol["grad"], dtype == torch.bfloat16)
+    check_close("dQ", f64(dq), dq_r, tol["grad"], dtype == torch.bfloat16, rel)
+    check_close("dK", f64(dk), dk_r, tol["grad"], dtype == torch.bfloat16, rel)
+    check_close("dV", f64(dv), dv_r, tol["grad"], dtype == torch.bfloat16, rel)
 
 
 def test_tiny_packed_fp32(gpu):

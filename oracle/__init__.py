@@ -6,5 +6,7 @@ binding never do, and share no code, header, table or helper with it.
 
   attention.py  softmax attention forward / backward / LSE merge (plain definitions)
   plan.py       reference tile classifier and work-list order
+  xent.py       softmax cross-entropy: loss, LSE and gradient (plain definition)
+  hdp.py        HDP planners: Eq. 3 offload ratio, Alg. 1, Alg. 2 (DP- and PP-Balance)
 """
 from . import attention, plan  # noqa: F401

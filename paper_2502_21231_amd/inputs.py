@@ -3,8 +3,9 @@
 This module only draws numbers and lays out indices: sequence-length mixes
 shaped after the paper's long-tailed datasets (Sec. 3.1, Observation 1, and the
 skew it reports), i.i.d. N(0,1) tensors, the token bookkeeping of the zig-zag
-packing layout (Sec. 7), and logits with labels for the cross-entropy.  It holds none of the attention arithmetic, and
-it imports neither the HIP binding nor the oracle.
+packing layout (Sec. 7), and logits with labels for the cross-entropy.  It holds
+none of the attention or cross-entropy arithmetic, and it imports neither the HIP
+binding nor the oracle.
 
 Tensors are drawn as float32 from ``numpy.random.default_rng([seed, tensor_id,
 chunk])`` over fixed 4 Mi-element chunks (so the values never depend on the

@@ -54,8 +54,10 @@ struct BwdParams {
   const bf16* k;
   const bf16* v;
   const bf16* dout;
+  const bf16* o;     // dQ kernel: the forward's output, for D = rowsum(dO * O)
   const float* lse;
   const float* dvec;
+  float* dvec_out;   // dQ kernel: where it stores D for the dK/dV kernel
   bf16* dq;          // varlen: dQ written directly
   float* dq_acc;     // chunk: dQ added into a float32 accumulator (dq == nullptr)
   bf16* dk;
@@ -102,17 +104,26 @@ void dq_bf16_kernel(const BwdParams p) {
   const int kvstride = p.hkv * D;
   const int64_t qoff = (int64_t)(it.a_start + (qvalid ? qrow : 0)) * qstride + (int64_t)h * D;
 
+  // Q and dO of this lane's row (its half of head_dim), and D = rowsum(dO * O) of the row
+  // (the two lanes of a row each sum their half; the dK/dV kernel reads D from dvec_out)
   bf16x8 qf[KK], dof[KK];
+  float dpart = 0.f;
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
     qf[kk] = *reinterpret_cast<const bf16x8*>(p.q + qoff + kk * 16 + hh * 8);
     dof[kk] = *reinterpret_cast<const bf16x8*>(p.dout + qoff + kk * 16 + hh * 8);
+    const bf16x8 ov = *reinterpret_cast<const bf16x8*>(p.o + qoff + kk * 16 + hh * 8);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) dpart = fmaf(bf2f(dof[kk][i]), bf2f(ov[i]), dpart);
   }
+  const float drow = half_sum(dpart);
   float lse2 = INFINITY, dval = 0.f;
   if (qvalid) {
-    const float l = p.lse[(int64_t)h * p.total_q + it.a_start + qrow];
+    const int64_t ri = (int64_t)h * p.total_q + it.a_start + qrow;
+    const float l = p.lse[ri];
     lse2 = l == -INFINITY ? INFINITY : l * kLog2e;
-    dval = p.dvec[(int64_t)h * p.total_q + it.a_start + qrow];
+    dval = drow;
+    if (hh == 0) p.dvec_out[ri] = drow;
   }
 
   const bf16* kbase = p.k + (int64_t)it.b_start * kvstride + (int64_t)hk * D;
@@ -485,11 +496,13 @@ BwdParams make_params(const bs_dims& dims, const void* q, const void* k, const v
 }  // namespace
 
 hipError_t launch_dq_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
-                          const void* dout, const float* lse, const float* dvec, int causal,
-                          float scale, void* dq, float* dq_acc, const void* ws, const WsLayout& L,
-                          hipStream_t stream) {
+                          const void* out, const void* dout, const float* lse, float* dvec,
+                          int causal, float scale, void* dq, float* dq_acc, const void* ws,
+                          const WsLayout& L, hipStream_t stream) {
   if (L.max_items == 0 || dims.hq == 0) return hipSuccess;
   BwdParams p = make_params(dims, q, k, v, dout, lse, dvec, causal, scale, ws, L);
+  p.o = static_cast<const bf16*>(out);
+  p.dvec_out = dvec;
   p.dq = static_cast<bf16*>(dq);
   p.dq_acc = dq_acc;
   const dim3 grid((unsigned)(L.max_items * dims.hq));

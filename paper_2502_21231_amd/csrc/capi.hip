@@ -325,9 +325,9 @@ int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
                     causal, ws, L, &Lp, s),
            "planner launch");
   }
-  {
+  if (f32) {  // the bf16 dQ kernel forms D itself
     ProfScope ps(BS_KERNEL_PREPROCESS, s);
-    BS_HIP(launch_bwd_preprocess(d, out, dout, dvec, (direct && f32) ? acc : nullptr, ws, s),
+    BS_HIP(launch_bwd_preprocess(d, out, dout, dvec, direct ? acc : nullptr, ws, s),
            "preprocess launch");
   }
   {
@@ -336,7 +336,7 @@ int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
       BS_HIP(launch_bwd_f32_dq(d, q, k, v, lse, dout, dvec, causal, scale, acc, ws, Lp, s),
              "backward dQ launch");
     else
-      BS_HIP(launch_dq_bf16(d, q, k, v, dout, lse, dvec, causal, scale, direct ? dq : nullptr,
+      BS_HIP(launch_dq_bf16(d, q, k, v, out, dout, lse, dvec, causal, scale, direct ? dq : nullptr,
                             acc, ws, Lp, s),
              "backward dQ launch");
   }

@@ -274,10 +274,12 @@ hipError_t launch_fwd_bf16(const bs_dims& dims, const void* q, const void* k, co
                            int causal, float scale, void* out, float* lse,
                            const FwdMerge* merge, const void* ws, const WsLayout& L,
                            hipStream_t stream);
+// The bf16 dQ kernel also forms D = rowsum(dO * O) and stores it in dvec for the dK/dV
+// kernel (the float32 path computes D in launch_bwd_preprocess).
 hipError_t launch_dq_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
-                          const void* dout, const float* lse, const float* dvec, int causal,
-                          float scale, void* dq, float* dq_acc, const void* ws, const WsLayout& L,
-                          hipStream_t stream);
+                          const void* out, const void* dout, const float* lse, float* dvec,
+                          int causal, float scale, void* dq, float* dq_acc, const void* ws,
+                          const WsLayout& L, hipStream_t stream);
 hipError_t launch_dkdv_bf16(const bs_dims& dims, const void* q, const void* k, const void* v,
                             const void* dout, const float* lse, const float* dvec, int causal,
                             float scale, void* dk, void* dv, int kv_accumulate, const void* ws,

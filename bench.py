@@ -3,9 +3,10 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
 A step is one causal attention forward + backward of the workload through the
-C ABI: device planning, forward, backward preprocess, backward, dQ finalize
-(and for the context-parallel workloads the per-step chunk calls plus the LSE
-merge, or the running merge of the ring rehearsal).  Two workloads measure the
+C ABI: device planning, forward, the dQ kernel (which also forms D =
+rowsum(dO * O)) and the dK/dV kernel (and for the context-parallel workloads the
+per-step chunk calls with their dQ finalize, plus the LSE merge, or the running
+merge of the ring rehearsal).  Two workloads measure the
 other rows of the build: hdp_batch7b (the HDP planners, checked by running every
 planned micro-batch) and xent_llama3_256k (the fused softmax cross-entropy, its
 own HBM metric).  Inputs are resident in HBM before timing starts; K steps are

@@ -21,8 +21,9 @@
 //                                    bf16 P that feeds its own products to its
 //                                    partner through LDS, and accumulates
 //                                    dV^T += dO^T P.
-//     dP wave (holds V of its keys): dP = dO V^T, dS = P (dP - D) with that
-//                                    bf16 P, dK^T += Q^T dS.
+//     dP wave (holds V of its keys): dP = dO V^T, then dP - D while the S wave
+//                                    is still on its exponentials; dS = P (dP - D)
+//                                    with that bf16 P, dK^T += Q^T dS.
 //   Row operands (Q for S, dO for dP) are row reads of the query tiles, the
 //   transposed ones (dO^T, Q^T) transposing LDS reads of the same tiles; P and
 //   dS feed the MFMA straight from registers.  Each wave keeps only one of the
@@ -402,20 +403,28 @@ void dkdv_bf16_kernel(const BwdParams p) {
 #pragma unroll
       for (int qs = 0; qs < QS; ++qs) pslot[qs * 64] = ob[qs];  // the bf16 P that feeds dV
     }
+    if (role == 1) {
+      // dP - D while the S wave is still on its exponentials (kept before the barrier)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) {
+          const f32x4 d4 = *reinterpret_cast<const f32x4*>(&Rb[BM + mb * 32 + a4 * 8 + hh * 4]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) s[mb][a4 * 4 + e] -= d4[e];
+        }
+        asm volatile("" : "+v"(s[mb]));
+      }
+    }
     barrier_lds();  // P of every key block is in LDS (the copies of tile i+1 stay in flight)
     if (role == 1) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const bf16x8 p0 = pslot[(mb * 2) * 64], p1 = pslot[(mb * 2 + 1) * 64];
 #pragma unroll
-        for (int a4 = 0; a4 < 4; ++a4) {
-          const f32x4 d4 = *reinterpret_cast<const f32x4*>(&Rb[BM + mb * 32 + a4 * 8 + hh * 4]);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = a4 * 4 + e;
-            const float pr = bf2f((r >> 3) == 0 ? p0[r & 7] : p1[r & 7]);
-            ob[mb * 2 + (r >> 3)][r & 7] = f2bf(pr * (s[mb][r] - d4[e]));
-          }
+        for (int r = 0; r < 16; ++r) {
+          const float pr = bf2f((r >> 3) == 0 ? p0[r & 7] : p1[r & 7]);
+          ob[mb * 2 + (r >> 3)][r & 7] = f2bf(pr * s[mb][r]);
         }
       }
     }

@@ -295,10 +295,11 @@ void dkdv_bf16_kernel(const BwdParams p) {
   const int diag = it.diag;
   const int n_iter = n_vis * p.group;
 
-  // All eight waves copy query tile i (head, rows) into QDd; the first dP wave
-  // fetches its LSE rows, the second its D rows (the other waves load a row too,
-  // unused, so that the copy has no branch and can be scheduled among the products).
-  const int ct = tid - 4 * 64;  // thread index among the role-1 waves
+  // All eight waves copy query tile i (head, rows) into QDd; the first S wave fetches its
+  // LSE rows, the second its D rows, and the S waves store them at the end of the step,
+  // where they wait for the dP waves anyway (the other waves load a row too, unused, so
+  // that the copy has no branch and can be scheduled among the products).
+  const int ct = tid;  // thread index among the role-0 waves
   float row_r = 0.f;   // raw LSE / D value of one row (converted when stored)
   bool row_ok = false;  // the row lies inside the segment
   auto copy_tile = [&](int i, bf16* QDd) {
@@ -327,7 +328,7 @@ void dkdv_bf16_kernel(const BwdParams p) {
 
   if (n_iter > 0) copy_tile(0, QD0);
   wait_vmem_all();  // K / V row, tile 0 and its rows
-  if (role == 1 && n_iter > 0) store_rows(R0);
+  if (role == 0 && n_iter > 0) store_rows(R0);
   __syncthreads();
 
   // phase 1 reads rows of Q (role 0) or dO (role 1); phase 2 reads dO (role 0)
@@ -447,7 +448,7 @@ void dkdv_bf16_kernel(const BwdParams p) {
       if (m + 3 < QS * DB) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 1);
     }
     wait_vmem_all();  // this wave's copies of tile i+1 and its rows
-    if (role == 1 && i + 1 < n_iter) store_rows(Rn);
+    if (role == 0 && i + 1 < n_iter) store_rows(Rn);
     __syncthreads();
   };
   for (int i = 0; i < n_iter; i += 2) {

@@ -108,6 +108,22 @@ def test_forward_is_bitwise_deterministic(gpu):
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+@pytest.mark.parametrize("hkv", [4, 1])
+def test_backward_is_bitwise_deterministic(gpu, hkv):
+    # no atomics: dQ is written once per query tile and dK, dV once per key tile (summed over
+    # the query heads of a KV group in a fixed order), so two runs agree bit for bit
+    lens = [300, 129, 64, 1]
+    T = sum(lens)
+    cu = torch.from_numpy(inputs.cu_seqlens(lens)).cuda()
+    q, k, v, do = make_qkv(11, T, T, 4, hkv, 128, torch.bfloat16)
+    qg, kg, vg, dog = to_gpu(q, k, v, do)
+    o, lse = B.bs_attn_varlen_fwd(qg, kg, vg, cu, cu, 300)
+    g1 = B.bs_attn_varlen_bwd(qg, kg, vg, o, lse, dog, cu, cu, 300)
+    g2 = B.bs_attn_varlen_bwd(qg, kg, vg, o, lse, dog, cu, cu, 300)
+    for name, a, b in zip(("dQ", "dK", "dV"), g1, g2):
+        assert torch.equal(a, b), name
+
+
 # ------------------------------------------------------------------ chunk mode
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_chunk_offsets_past_diagonal_straddle_future(gpu, dtype):

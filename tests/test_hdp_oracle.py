@@ -1,7 +1,9 @@
 """Pins of the HDP planner oracle (Sec. 5, Sec. 6) against what the paper and the mathematics fix:
 the rank counts the paper works out, closed forms of Eq. 3 at r = 0, r = 1 and an exact
 intermediate ratio, a brute-force argmin of Eq. 3, a hand-worked best-fit packing, the any-fit
-property and brute-force optimal bin counts, and the invariants of both assignments."""
+property and brute-force optimal bin counts, Alg. 2 traced by hand (the equal-FLOPs bucket cut,
+DP-Balance and PP-Balance plans unit by unit, a context-parallel unit), Insight 1's one length
+level per pipeline, and the invariants of every assignment."""
 import itertools
 import math
 
@@ -184,3 +186,117 @@ def test_rejects_a_sequence_wider_than_the_ranks():
         H.naive_hdp([10 * 1024], 1024, 4, cost(bw=0.0))
     with pytest.raises(ValueError):
         H.balance([10 * 1024], 1024, 4, cost(bw=0.0), 0.0, H.ALG_DP_BALANCE, 2)
+
+
+# ---------------------------------------------------------------------------------------------
+# Alg. 2 (Sec. 6.4) traced by hand.  T(s) = s (alpha1 = 0, beta1 = 1, gamma = 0) keeps every
+# finish time an integer; with no host bandwidth a long sequence of s tokens takes
+# D = ceil(s / C) ranks (Eq. 3 at r = 0) and T(s) / D on each.
+
+def linear_cost():
+    return cost(alpha1=0.0, beta1=1.0, gamma=0.0, alpha2=1.0, beta2=0.0, bw=0.0)
+
+
+def test_buckets_cut_by_equal_cost_not_by_count():
+    """Step 1 of Alg. 2: the length-sorted batch is cut into runs of about equal total FLOPs, so a
+    bucket of longer sequences holds fewer of them.  Lengths (by index) 1 8 2 1 4 1 1, sorted
+    8 4 2 1 1 1 1 (indices 1 4 2 0 3 5 6), total cost 18, 2 buckets: the cost before each sequence
+    is 0 8 12 14 15 16 17 and a sequence falls into bucket floor(2 * before / 18), which gives
+    {8, 4} (cost 12) and {2, 1, 1, 1, 1} (cost 6).  A cut into equal counts would give {8, 4, 2, 1}
+    and {1, 1, 1}, whose longer bucket holds more sequences.  With T(s) = s^2 the costs are
+    64 16 4 1 1 1 1 (total 88; before: 0 64 80 84 85 86 87) and the first bucket is {8} alone."""
+    lengths = [1, 8, 2, 1, 4, 1, 1]
+    assert H._buckets(lengths, linear_cost(), 2) == [[1, 4], [2, 0, 3, 5, 6]]
+    quad = cost(alpha1=1.0, beta1=0.0, gamma=0.0, alpha2=1.0, bw=0.0)
+    assert H._buckets(lengths, quad, 2) == [[1], [4, 2, 0, 3, 5, 6]]
+    # three buckets, T(s) = s: floor(3 * before / 18) = floor(before / 6) -> 0 1 2 2 2 2 2
+    assert H._buckets(lengths, linear_cost(), 3) == [[1], [4], [2, 0, 3, 5, 6]]
+
+
+def test_buckets_are_equal_cost_runs_on_random_batches():
+    """On seeded random batches: the buckets are consecutive runs of the length-sorted batch; a
+    bucket's cost differs from total / n_b by less than the largest single cost; and the bucket
+    of the longest sequences holds fewer of them than the bucket of the shortest."""
+    rng = np.random.default_rng(21)
+    for _ in range(60):
+        n = int(rng.integers(8, 120))
+        L = [int(x) for x in rng.integers(1, 5000, n)]
+        c = cost(alpha1=float(rng.uniform(0, 1e-9)), beta1=float(rng.uniform(1e-8, 1e-6)),
+                 gamma=float(rng.uniform(0, 1e-6)), bw=0.0)
+        nb = int(rng.integers(2, 6))
+        B = H._buckets(L, c, nb)
+        flat = [i for b in B for i in b]
+        assert flat == sorted(range(n), key=lambda i: (-L[i], i))
+        costs = [sum(c.T(L[i]) for i in b) for b in B]
+        tot, top = sum(c.T(x) for x in L), max(c.T(x) for x in L)
+        for cb in costs:
+            assert abs(cb - tot / nb) < top + 1e-12 * tot
+        assert len(B[0]) < len(B[-1]), [len(x) for x in B]
+
+
+def test_dp_balance_traced_by_hand():
+    """Lengths 6 5 4 3 3 2 2 1 1 1, C = 6, three ranks, delta = 1.5, two buckets (cost before each
+    sequence 0 6 11 15 18 21 23 25 26 27 of 28: B0 = {0, 1, 2}, B1 = {3 .. 9}).  DP-Balance takes
+    every unit from the first bucket:
+      round 1  nobody lags (all at 0): rank 0 (first to finish) gets {0}            -> 6 0 0
+      round 2  max 6, lagging 1, 2:   rank 1 gets {1}                             -> 6 5 0
+               lagging 2:             rank 2 gets {2}, B0 empties                 -> 6 5 4
+               lagging 2 (6-4 > 1.5): rank 2 gets {3, 4} (first fit in C = 6)     -> 6 5 10
+      round 3  max 10, lagging 1, 0:  rank 1 gets {5, 6, 7, 8}                    -> 6 11 10
+               lagging 0:             rank 0 gets {9}, B1 empties                 -> 7 11 10"""
+    lengths = [6, 5, 4, 3, 3, 2, 2, 1, 1, 1]
+    out, rt = H.balance(lengths, 6, 3, linear_cost(), 1.5, H.ALG_DP_BALANCE, 2)
+    assert [(s, g, st, t) for s, g, _, st, t in out] == [
+        ((0,), (0,), 0.0, 6.0), ((1,), (1,), 0.0, 5.0), ((2,), (2,), 0.0, 4.0),
+        ((3, 4), (2,), 4.0, 6.0), ((5, 6, 7, 8), (1,), 5.0, 6.0), ((9,), (0,), 6.0, 1.0)]
+    assert rt == [7.0, 11.0, 10.0]
+
+
+def test_pp_balance_draws_rank_g_from_bucket_g_mod_nb():
+    """The same batch under PP-Balance: rank g takes its unit from bucket g mod #buckets, so each
+    pipeline stays on one length level while every bucket lasts (Sec. 6.2, Insight 1); once B0
+    empties, every rank draws from the one bucket left:
+      round 1  nobody lags: rank 0 <- B0: {0}                                    -> 6 0 0
+      round 2  lagging 1, 2: rank 1 <- B1: {3, 4}                               -> 6 6 0
+               lagging 2:    rank 2 <- B0 (2 mod 2): {1}                         -> 6 6 5
+      round 3  max 6, nobody lags by more than 1.5: rank 2 <- B0: {2}, B0 empties -> 6 6 9
+      round 4  max 9, lagging 0, 1: rank 0 <- B1 (0 mod 1): {5, 6, 7, 8}         -> 12 6 9
+               lagging 1:    rank 1 <- B1: {9}                                   -> 12 7 9"""
+    lengths = [6, 5, 4, 3, 3, 2, 2, 1, 1, 1]
+    out, rt = H.balance(lengths, 6, 3, linear_cost(), 1.5, H.ALG_PP_BALANCE, 2)
+    assert [(s, g, st, t) for s, g, _, st, t in out] == [
+        ((0,), (0,), 0.0, 6.0), ((3, 4), (1,), 0.0, 6.0), ((1,), (2,), 0.0, 5.0),
+        ((2,), (2,), 5.0, 4.0), ((5, 6, 7, 8), (0,), 6.0, 6.0), ((9,), (1,), 6.0, 1.0)]
+    assert rt == [12.0, 7.0, 9.0]
+
+
+def test_balance_places_a_context_parallel_unit_on_the_first_free_ranks():
+    """Lengths 9 3 2 2 1, C = 4, three ranks, delta = 1.5, two buckets (before: 0 9 12 14 16 of 17:
+    B0 = {0}, B1 = {1 .. 4}).  Sequence 0 needs ceil(9 / 4) = 3 ranks at T / 3 = 3 each:
+      round 1  nobody lags: rank 0 draws {0}, a CP unit on ranks 0 1 2 from 0     -> 3 3 3
+      round 2  nobody lags: rank 0 <- {1, 4} (3 + 1 fill C = 4)                   -> 7 3 3
+      round 3  max 7, lagging 1, 2: rank 1 <- {2, 3}, the last bucket empties     -> 7 7 3"""
+    out, rt = H.balance([9, 3, 2, 2, 1], 4, 3, linear_cost(), 1.5, H.ALG_DP_BALANCE, 2)
+    assert [(s, g, st, t) for s, g, _, st, t in out] == [
+        ((0,), (0, 1, 2), 0.0, 3.0), ((1, 4), (0,), 3.0, 4.0), ((2, 3), (1,), 3.0, 4.0)]
+    assert rt == [7.0, 7.0, 3.0]
+
+
+def test_pp_balance_keeps_each_pipeline_on_one_length_level():
+    """Insight 1 (Sec. 6.2) on seeded batches of short sequences with as many ranks as buckets:
+    until the first bucket runs out, every unit rank g receives comes from bucket g, the g-th
+    length level, so the units of different ranks never mix levels."""
+    c = cost(alpha1=2e-11, beta1=5e-8, gamma=1e-5, alpha2=4e5, layers=32, bw=5e10)
+    C, nb = 32 * K, 4
+    for seed in range(4):
+        lengths = [min(x, C) for x in lognormal_batch(200 + seed, 400, C)]
+        B = H._buckets(lengths, c, nb)
+        level = {i: b for b, bucket in enumerate(B) for i in bucket}
+        out, _ = H.balance(lengths, C, nb, c, 1e-4, H.ALG_PP_BALANCE, nb)
+        sizes = [len(b) for b in B]
+        taken = [0] * len(B)
+        for seqs, (g,), *_ in out:
+            if any(taken[b] == sizes[b] for b in range(len(B))):
+                break  # a bucket ran out: the rank -> bucket map shifts from here on
+            assert {level[i] for i in seqs} == {g}, (seed, seqs, g)
+            taken[g] += len(seqs)

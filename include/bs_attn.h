@@ -28,7 +28,8 @@
  * Conventions for every entry point
  *   - All tensor pointers are DEVICE pointers, contiguous, owned by the caller.
  *     The library never allocates device memory on a call; scratch space comes
- *     from a caller-provided workspace sized by bs_attn_workspace_size().
+ *     from a caller-provided workspace sized by bs_attn_workspace_size(), except
+ *     for bs_attn_varlen_fwd_noalloc(), which plans into a fixed device array.
  *   - Layouts (row-major):  Q, O, dO, dQ: [T, hq, head_dim];
  *     K, V, dK, dV: [Tk, hkv, head_dim];  LSE and D: float32 [hq, T];
  *     merge partials: O [n, T, hq, head_dim], LSE [n, hq, T]; running merge
@@ -121,6 +122,33 @@ int bs_attn_varlen_fwd(const bs_dims* dims, const void* q, const void* k, const 
                        int32_t num_seqs, int32_t max_seqlen, int causal, float scale,
                        void* out, float* lse, void* workspace, size_t workspace_bytes,
                        void* stream);
+
+/* Bytes of the per-device scratch array behind bs_attn_varlen_fwd_noalloc(). */
+#define BS_NOALLOC_SCRATCH_BYTES ((size_t)4 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): bs_attn_varlen_fwd without the
+ * workspace arguments.  Same computation, arguments, layouts and results as
+ * bs_attn_varlen_fwd; the plan that the forward kernel walks goes into a file-scope
+ * device array of BS_NOALLOC_SCRATCH_BYTES (4 MiB) that the library holds on every
+ * device it runs on until the process ends.  No hipMalloc or hipFree, and no allocating
+ * library routine, is called.
+ *   - Limit: the plan takes 256 B + 4 (2 num_seqs + 3) B (each part rounded up to 256 B)
+ *     + 48 B per work item, with ceil(total_q / 128) + num_seqs items (bf16) or
+ *     ceil(total_q / 64) + num_seqs items (float32); sizes beyond the array return
+ *     BS_ERR_WORKSPACE (for example about 11M bf16 query tokens in 20 segments) and
+ *     enqueue nothing.
+ *   - `stream` must belong to the current device (BS_ERR_INVALID_ARG otherwise); the
+ *     first call on a device looks up the array's address there (hipGetSymbolAddress).
+ *   - Every call on one device uses that device's one array: calls that can overlap on
+ *     a device (different streams, or other host threads) race and must be ordered by
+ *     the caller.  The array keeps the last call's plan; nothing in it needs clearing.
+ *   - A cu_seqlens error found on the device is written into the array's status word,
+ *     which no helper reads: out and lse are then left unwritten. */
+int bs_attn_varlen_fwd_noalloc(const bs_dims* dims, const void* q, const void* k, const void* v,
+                               const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                               int32_t num_seqs, int32_t max_seqlen, int causal, float scale,
+                               void* out, float* lse, void* stream);
 
 /* Varlen backward: given the forward's out and lse and the upstream gradient
  * dout, writes dq [T, hq, d], dk and dv [Tk, hkv, d] (overwritten, not added).

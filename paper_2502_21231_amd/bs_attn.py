@@ -29,7 +29,9 @@ EXPORTS = (
     "bs_softmax_xent",
     "bs_dq_finalize", "bs_lse_merge", "bs_read_device_status",
     "bs_attn_plan_export", "bs_set_profiling", "bs_profile_read", "bs_last_error",
+    "bs_attn_varlen_fwd_noalloc",
 )
+BS_NOALLOC_SCRATCH_BYTES = 4 << 20  # the per-device plan scratch of bs_attn_varlen_fwd_noalloc
 (BS_KERNEL_PLAN, BS_KERNEL_FWD, BS_KERNEL_PREPROCESS, BS_KERNEL_BWD_DQ, BS_KERNEL_BWD_DKDV,
  BS_KERNEL_FINALIZE, BS_KERNEL_MERGE, BS_KERNEL_XENT) = range(8)
 
@@ -63,6 +65,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "bs_attn_workspace_size": (_SZ, [ctypes.c_int, _DIMS, _I32, _I32]),
         "bs_attn_varlen_fwd": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _I32, _I32, ctypes.c_int, _F,
                                               _P, _P, _P, _SZ, _P]),
+        "bs_attn_varlen_fwd_noalloc": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _I32, _I32,
+                                                      ctypes.c_int, _F, _P, _P, _P]),
         "bs_attn_varlen_bwd": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _P, _P, _I32, _I32,
                                               ctypes.c_int, _F, _P, _P, _P, _P, _SZ, _P]),
         "bs_attn_chunk_fwd": (ctypes.c_int, [_DIMS, _P, _P, _P, _I64, _I64, ctypes.c_int, _F, _P, _P,
@@ -191,6 +195,28 @@ def bs_attn_varlen_fwd(q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen: int, cau
         ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_q), _ptr(cu_seqlens_k), nseq,
         int(max_seqlen), int(bool(causal)), _scale(scale, q.shape[2]), _ptr(out), _ptr(lse),
         _ptr(workspace), workspace.numel(), _stream(q.device)))
+    return out, lse
+
+
+def bs_attn_varlen_fwd_noalloc(q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen: int,
+                               causal: bool = True, scale: float | None = None, out=None, lse=None):
+    """bs_attn_varlen_fwd with no workspace: the library plans into its own per-device scratch
+    array.  Pass preallocated out / lse to make the call allocate nothing at all."""
+    _qkv(q, k, v)
+    _need(cu_seqlens_q, "cu_seqlens_q", torch.int32, 1)
+    _need(cu_seqlens_k, "cu_seqlens_k", torch.int32, 1)
+    if cu_seqlens_q.numel() != cu_seqlens_k.numel():
+        raise ValueError("cu_seqlens_q and cu_seqlens_k must have the same length")
+    dims = make_dims(q, k)
+    nseq = cu_seqlens_q.numel() - 1
+    out = torch.empty_like(q) if out is None else out
+    lse = torch.empty(q.shape[1], q.shape[0], dtype=torch.float32, device=q.device) if lse is None else lse
+    _need(out, "out", q.dtype)
+    _need(lse, "lse", torch.float32)
+    _check(load_library().bs_attn_varlen_fwd_noalloc(
+        ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_q), _ptr(cu_seqlens_k), nseq,
+        int(max_seqlen), int(bool(causal)), _scale(scale, q.shape[2]), _ptr(out), _ptr(lse),
+        _stream(q.device)))
     return out, lse
 
 

@@ -11,6 +11,13 @@
 
 #include "common.hpp"
 
+// Scratch of the allocation-free forward (bs_attn_varlen_fwd_noalloc): the plan that the
+// forward kernel walks (header, per-segment offsets, work list).  Each device holds its own
+// copy from the time the library's code is loaded on it until the process ends.  Host code
+// never uses this name as an address: the device address comes from hipGetSymbolAddress.
+constexpr size_t kNoAllocScratchBytes = BS_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace bs {
 namespace {
 
@@ -364,6 +371,36 @@ int bwd_common(int op, const bs_dims* dims, const void* q, const void* k, const 
   return ok();
 }
 
+// Device address of `scratch` on each device, looked up once per device (with that device
+// current) on the first allocation-free call made there.
+constexpr int kMaxScratchDevices = 256;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxScratchDevices] = {};
+
+int noalloc_scratch(void* stream, void** addr) {
+  int dev = -1;
+  BS_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (stream != nullptr) {
+    int sdev = -1;
+    BS_HIP(hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev), "hipStreamGetDevice");
+    if (sdev != dev)
+      return fail(BS_ERR_INVALID_ARG, "stream belongs to device %d but device %d is current", sdev,
+                  dev);
+  }
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(BS_ERR_UNSUPPORTED, "device %d is beyond the %d devices with scratch slots", dev,
+                kMaxScratchDevices);
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (g_scratch_addr[dev] == nullptr) {
+    void* p = nullptr;
+    BS_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (p == nullptr) return fail(BS_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_addr[dev] = p;
+  }
+  *addr = g_scratch_addr[dev];
+  return BS_OK;
+}
+
 }  // namespace
 }  // namespace bs
 
@@ -392,6 +429,26 @@ int bs_attn_varlen_fwd(const bs_dims* dims, const void* q, const void* k, const 
   return fwd_common(BS_OP_VARLEN_FWD, dims, q, k, v, cu_seqlens_q, cu_seqlens_k, nullptr, nullptr,
                     num_seqs, max_seqlen, 0, 0, causal, scale, out, lse, nullptr, workspace,
                     workspace_bytes, stream);
+}
+
+int bs_attn_varlen_fwd_noalloc(const bs_dims* dims, const void* q, const void* k, const void* v,
+                               const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                               int32_t num_seqs, int32_t max_seqlen, int causal, float scale,
+                               void* out, float* lse, void* stream) {
+  BS_TRY(check_dims(dims, true));
+  BS_TRY(check_varlen_args(BS_OP_VARLEN_FWD, cu_seqlens_q, cu_seqlens_k, nullptr, nullptr,
+                           num_seqs, max_seqlen));
+  const size_t need = layout_of(BS_OP_VARLEN_FWD, *dims, num_seqs).total;
+  if (need > kNoAllocScratchBytes)
+    return fail(BS_ERR_WORKSPACE,
+                "these sizes need %zu bytes of plan scratch, more than the %zu bytes of the "
+                "allocation-free forward (use bs_attn_varlen_fwd with a workspace)",
+                need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  BS_TRY(noalloc_scratch(stream, &ws));
+  return fwd_common(BS_OP_VARLEN_FWD, dims, q, k, v, cu_seqlens_q, cu_seqlens_k, nullptr, nullptr,
+                    num_seqs, max_seqlen, 0, 0, causal, scale, out, lse, nullptr, ws,
+                    kNoAllocScratchBytes, stream);
 }
 
 int bs_attn_varlen_bwd(const bs_dims* dims, const void* q, const void* k, const void* v,

@@ -27,7 +27,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 18, names
+    assert len(names) == 19, names
     assert set(names) == set(B.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
@@ -152,3 +152,16 @@ def test_workspace_size_grows_with_problem(lib):
     pk = B.bs_attn_workspace_size(B.BS_OP_PACKED_CHUNK_BWD,
                                   dims(total_q=4096, total_k=4096, dtype=B.BS_F32), 1, 4096)
     assert bwd <= pk < f32
+
+
+def test_noalloc_forward_rejects_sizes_beyond_its_scratch(lib):
+    """The allocation-free forward checks the plan size against its fixed scratch array on the
+    host and enqueues nothing: 2^28 bf16 query tokens need 2M work items of 48 B."""
+    def call(d, n=1, cu=FAKE):
+        return lib.bs_attn_varlen_fwd_noalloc(ctypes.byref(d), FAKE, FAKE, FAKE, cu, cu, n, 1 << 28,
+                                              1, 0.1, FAKE, FAKE, None)
+    assert call(dims(total_q=1 << 28, total_k=1 << 28)) == B.BS_ERR_WORKSPACE
+    assert "allocation-free" in B.bs_last_error()
+    assert call(dims(head_dim=96)) == B.BS_ERR_UNSUPPORTED
+    assert call(dims(), cu=None) == B.BS_ERR_INVALID_ARG
+    assert call(dims(), n=-1) == B.BS_ERR_INVALID_ARG

@@ -220,38 +220,98 @@ def time_steps(step, args, dev, flops_fwd, flops_bwd):
     }
 
 
-CPU_BASELINE_HEADS = 6  # query heads the oracle runs (about 10-15 s of float64 work on 16 cores)
+# The CPU oracle runs on a bounded sample of each workload (about 10-30 s of float64 work on
+# the GPU machine's 16 host cores), so that a default benchmark run stays within minutes; the
+# full-problem time is extrapolated from it and labelled as such.  The oracle computes every
+# (row, key) score of a segment or chunk and masks it, so its time is proportional to
+# rows x keys x query heads (not to the visible pairs): that is the extrapolation factor.
+CPU_BASELINE_HEADS = 6  # packed7b: query heads 0..5 of 32 over every segment (about 14 s)
+CPU_BASELINE_CHUNK_ROWS = {"cp7b": 2048, "zigzag141b": 1024}  # Q rows per part, KV group 0
+CPU_BASELINE_GQA_AREA = 8e8  # gqa70b: rows x keys x query heads of KV group 0's sample
+
+
+def blas_cores():
+    try:
+        import threadpoolctl
+        return int(max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()
+                       if i.get("user_api") == "blas"))
+    except Exception:
+        return len(os.sched_getaffinity(0))
 
 
 def cpu_baseline_varlen(W, scale):
-    """The float64 oracle on the first query heads of the same workload (fwd + bwd, all segments)."""
+    """The float64 oracle (fwd + bwd) on a sample of the same workload: the first query heads
+    over every segment when a KV group is a single head (MHA); otherwise KV group 0 (all its
+    query heads) over every segment but the longest."""
     import numpy as np
-    import torch
     from oracle import attention as A
-    try:
-        import threadpoolctl
-        cores = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()
-                    if i.get("user_api") == "blas")
-    except Exception:
-        cores = len(os.sched_getaffinity(0))
     hq, hkv, d = W["hq"], W["hkv"], W["d"]
     g = hq // hkv
-    H = min(CPU_BASELINE_HEADS, hq)
+    lens = W["lens"]
+    if g == 1:
+        H, segs = min(CPU_BASELINE_HEADS, hq), list(range(len(lens)))
+    else:  # the segments in order, skipping the longest, within the sample's budget of work
+        longest = int(np.argmax(lens))
+        H, segs, area = g, [], 0
+        for b in range(len(lens)):
+            if b != longest and area + g * lens[b] ** 2 <= CPU_BASELINE_GQA_AREA:
+                segs.append(b)
+                area += g * lens[b] ** 2
     Hk = (H - 1) // g + 1  # the KV heads those query heads read
-    q = W["q_cpu"][:, :H]
-    k = W["k_cpu"][:, :Hk]
-    v = W["v_cpu"][:, :Hk]
-    do = W["do_cpu"][:, :H]
-    cu = W["cu_cpu"].numpy()
+    cu_all = W["cu_cpu"].numpy()
+    rows = np.concatenate([np.arange(cu_all[b], cu_all[b + 1]) for b in segs])
+    sl = np.array([lens[b] for b in segs], dtype=np.int64)
+    cu = np.concatenate([[0], np.cumsum(sl)]).astype(np.int32)
+    q = W["q_cpu"][rows, :H]
+    k = W["k_cpu"][rows, :Hk]
+    v = W["v_cpu"][rows, :Hk]
+    do = W["do_cpu"][rows, :H]
     t0 = time.perf_counter()
     o, l = A.varlen_fwd(q, k, v, cu, cu, True, scale)
     A.varlen_bwd(q, k, v, o, l, do, cu, cu, True, scale)
     dt = time.perf_counter() - t0
-    flops = 14 * d * H * W["A"]
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"query heads 0..{H - 1} of {hq} (KV heads 0..{Hk - 1}), all {len(W['lens'])} "
-                      f"segments, fwd+bwd in float64 NumPy: {flops:.3e} FLOP in {dt:.1f} s",
-            "seconds": dt}
+    a_s = int(sum(x * (x + 1) // 2 for x in sl))
+    flops = 14 * d * H * a_s
+    area_s = float(sum(x * x for x in sl)) * H
+    area_full = float(sum(x * x for x in lens)) * hq
+    what = (f"query heads 0..{H - 1} of {hq} (KV heads 0..{Hk - 1}) over "
+            + (f"all {len(lens)} segments" if len(segs) == len(lens)
+               else f"{len(segs)} of {len(lens)} segments (in order, the longest left out)"))
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": blas_cores(), "kind": "oracle",
+            "sample": f"{what}, fwd+bwd in float64 NumPy: {flops:.3e} FLOP in {dt:.1f} s",
+            "seconds": dt, "extrapolated_full_seconds": dt * area_full / area_s,
+            "extrapolation": "extrapolated: sample time x (rows x keys x query heads of the full "
+                             "problem) / (the same of the sample)"}
+
+
+def cpu_baseline_chunk(name, Qs, dOs, Ks, Vs, q_offs, kv_offs, pairs, hq, hkv, c, scale):
+    """The float64 oracle on KV group 0 (its query heads) and the first rows of every Q part of a
+    context-parallel share: per-step chunk forward, LSE merge, per-step chunk backward.  Qs, dOs:
+    the sampled rows [R, G, d] of each Q part; Ks, Vs: KV head 0 [c, 1, d] of each KV part."""
+    import numpy as np
+    from oracle import attention as A
+    d = Qs[0].shape[2]
+    g = hq // hkv
+    R = Qs[0].shape[0]
+    per_q = {i: [j for (a, j) in pairs if a == i] for i in range(len(q_offs))}
+    t0 = time.perf_counter()
+    for i, js in per_q.items():
+        outs = [A.chunk_fwd(Qs[i], Ks[j], Vs[j], q_offs[i], kv_offs[j], True, scale) for j in js]
+        o, l = A.lse_merge(np.stack([x[0] for x in outs]), np.stack([x[1] for x in outs]))
+        for j in js:
+            A.chunk_bwd(Qs[i], Ks[j], Vs[j], o, l, dOs[i], q_offs[i], kv_offs[j], True, scale)
+    dt = time.perf_counter() - t0
+    a_s = sum(visible_pairs_chunk_closed(R, c, q_offs[i] - kv_offs[j]) for i, j in pairs)
+    flops = 14 * d * g * a_s
+    scale_up = (c / R) * (hq / g)  # every row of a part costs the same: rows x keys x heads
+    return {"value": flops / dt / 1e12 if dt > 0 else None, "unit": "TFLOP/s", "cores": blas_cores(),
+            "kind": "oracle",
+            "sample": f"KV group 0 (query heads 0..{g - 1} of {hq}), the first {R} of {c} rows of "
+                      f"each of {len(q_offs)} Q part(s) against all {len(kv_offs)} KV part(s) "
+                      f"({len(pairs)} steps), fwd + merge + bwd in float64 NumPy: {flops:.3e} FLOP "
+                      f"({a_s} visible pairs per head) in {dt:.1f} s",
+            "seconds": dt, "extrapolated_full_seconds": dt * scale_up,
+            "extrapolation": f"extrapolated: sample time x {c}/{R} rows x {hq}/{g} query heads"}
 
 
 def chunk_workload(name):
@@ -276,10 +336,20 @@ def run_chunk_bench(args, dev):
     hq, hkv, c, q_offs, kv_offs, pairs = chunk_workload(args.workload)
     d, seed = 128, args.seed
     scale = 1.0 / math.sqrt(d)
-    Q = [inputs.normal(seed, inputs.TID_Q + 100 * i, (c, hq, d)).to(dev) for i in range(len(q_offs))]
-    dO = [inputs.normal(seed, inputs.TID_DO + 100 * i, (c, hq, d)).to(dev) for i in range(len(q_offs))]
-    K = [inputs.normal(seed, inputs.tid_chunk_k(j), (c, hkv, d)).to(dev) for j in range(len(kv_offs))]
-    V = [inputs.normal(seed, inputs.tid_chunk_v(j), (c, hkv, d)).to(dev) for j in range(len(kv_offs))]
+    g = hq // hkv
+    R = CPU_BASELINE_CHUNK_ROWS[args.workload]
+    sample = {"Q": [], "dO": [], "K": [], "V": []}  # the CPU oracle's rows: KV group 0
+
+    def load(tid, shape, key, rows, heads):
+        t = inputs.normal(seed, tid, shape)
+        if args.cpu_baseline:
+            sample[key].append(t[:rows, :heads].clone())
+        return t.to(dev)
+
+    Q = [load(inputs.TID_Q + 100 * i, (c, hq, d), "Q", R, g) for i in range(len(q_offs))]
+    dO = [load(inputs.TID_DO + 100 * i, (c, hq, d), "dO", R, g) for i in range(len(q_offs))]
+    K = [load(inputs.tid_chunk_k(j), (c, hkv, d), "K", c, 1) for j in range(len(kv_offs))]
+    V = [load(inputs.tid_chunk_v(j), (c, hkv, d), "V", c, 1) for j in range(len(kv_offs))]
     dims = B.make_dims(Q[0], K[0])
     ws_f = B.alloc_workspace(B.BS_OP_CHUNK_FWD, dims, dev)
     ws_b = B.alloc_workspace(B.BS_OP_CHUNK_BWD, dims, dev)
@@ -336,6 +406,10 @@ def run_chunk_bench(args, dev):
         n = len(per_q[0])
         nbytes = n * c * hq * d * 2 + n * hq * c * 4 + c * hq * d * 2 + hq * c * 4
         res["lse_merge_gbs"] = nbytes / (merge["avg_ms_per_launch"] * 1e-3) / 1e9
+        res["lse_merge_bytes"] = nbytes
+    if args.cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_chunk(args.workload, sample["Q"], sample["dO"], sample["K"],
+                                                 sample["V"], q_offs, kv_offs, pairs, hq, hkv, c, scale)
     return res
 
 
@@ -447,6 +521,7 @@ def run_zigzag_packed_bench(args, dev):
     if merge:
         nbytes = n * Tq * hq * d * 2 + n * hq * Tq * 4 + Tq * hq * d * 2 + hq * Tq * 4
         res["lse_merge_gbs"] = nbytes / (merge["avg_ms_per_launch"] * 1e-3) / 1e9
+        res["lse_merge_bytes"] = nbytes
     return res
 
 
@@ -778,6 +853,7 @@ def main():
         "kernels": res["kernels"], "flops_per_step": res["flops_per_step"],
         "roofline": res["roofline"],
         "lse_merge_gbs": res.get("lse_merge_gbs"),
+        "lse_merge_bytes": res.get("lse_merge_bytes"),
         "ring_copies": res.get("ring_copies"),
         "hdp": res.get("hdp"),
         "cpu_baseline": res.get("cpu_baseline"),

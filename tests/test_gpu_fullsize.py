@@ -4,6 +4,9 @@ The oracle cannot redo a whole 32K..131K-token problem in seconds, so it checks
   * sampled query rows one by one (O, LSE, dQ): a row needs only its own keys;
   * sampled keys near the end of a segment or diagonal chunk (dK, dV): only the few
     query rows after them see them, so the oracle needs only those rows;
+  * sampled early keys of the longest segments and of past chunks (dK, dV): tens of
+    thousands of query rows accumulate into them; the oracle sums over exactly those
+    rows, with the GPU's row-checked O and LSE as its inputs;
 and every output is checked against properties that hold at any size: per segment
 (or per query shard) and KV head, sum_j dK_j = 0 and sum_j dV_j = sum over the group's
 query heads of sum_i dO_i (the rows of P sum to 1, the rows of dS to 0).
@@ -35,6 +38,18 @@ def row_oracle(qrow, K, V, dorow, q_pos, k_pos):
     o_in = torch.from_numpy(o).to(BF)
     dq, _, _ = A.chunk_bwd(qrow, K, V, o_in, l, dorow, q_pos, k_pos, True, SCALE)
     return o, l, dq
+
+
+def key_oracle(row_sets, kj, vj, k_pos):
+    """dK, dV [d] of one key (kj, vj: [1, 1, d] at global position k_pos) from every query row
+    that sees it: row_sets lists (q [r, G, d], dO [r, G, d], O [r, G, d], LSE [G, r], first row's
+    position) of the group's query heads, with the GPU's row-checked O and LSE as the backward's
+    inputs (the chunk backward of a one-key chunk sums dS q and P dO over exactly those rows)."""
+    gk, gv = 0.0, 0.0
+    for qb, dob, ob, lb, q_pos in row_sets:
+        _, a, b = A.chunk_bwd(qb, kj, vj, ob, lb, dob, q_pos, k_pos, True, SCALE)
+        gk, gv = gk + a[0, 0], gv + b[0, 0]
+    return gk, gv
 
 
 def check_grad_sums(name, dk, dv, do, hq, hkv, key_ranges, row_ranges):
@@ -95,6 +110,18 @@ def varlen_fullsize(lens, hq, hkv, seed):
             _, gk, gv = A.chunk_bwd(qb, K, V, torch.from_numpy(o).to(BF), l, dob, r0, 0, True, SCALE)
             check_close(f"dK seg{b} hk{hk}", f64(dk_c[s + r0:s + L, hk:hk + 1]), gk[r0:], 2e-2, True)
             check_close(f"dV seg{b} hk{hk}", f64(dv_c[s + r0:s + L, hk:hk + 1]), gv[r0:], 2e-2, True)
+    # dK, dV of early keys of the two longest segments, KV head 0 and the last one: every query
+    # row of the segment from the key on (thousands of FULL query tiles) accumulates into them
+    for b in [int(x) for x in order[:2]]:
+        s, L = int(cu[b]), lens[b]
+        for j in sorted({0, 1, min(L - 1, 127), min(L - 1, 128), L // 2}):
+            for hk in sorted({0, hkv - 1}):
+                hs = slice(hk * G, (hk + 1) * G)
+                gk, gv = key_oracle([(q[s + j:s + L, hs], do[s + j:s + L, hs], out_c[s + j:s + L, hs],
+                                      lse_c[hs, s + j:s + L], j)], k[s + j:s + j + 1, hk:hk + 1],
+                                    v[s + j:s + j + 1, hk:hk + 1], j)
+                check_close(f"dK seg{b} key{j} hk{hk}", f64(dk_c[s + j, hk]), gk, 2e-2, True)
+                check_close(f"dV seg{b} key{j} hk{hk}", f64(dv_c[s + j, hk]), gv, 2e-2, True)
     ranges = [(int(cu[b]), int(cu[b + 1])) for b in range(len(lens))]
     check_grad_sums("varlen", dk_c, dv_c, do, hq, hkv, ranges, ranges)
 
@@ -205,6 +232,26 @@ def chunk_share_check(Q, dO, K, V, O, L, dQ, dK, dV, hq, hkv, q_offs, kv_offs, p
                                         SCALE)
                 check_close(f"dK kv{j} hk{hk}", f64(dK[j][r0:, hk:hk + 1]), gk[r0:], 2e-2, True)
                 check_close(f"dV kv{j} hk{hk}", f64(dV[j][r0:, hk:hk + 1]), gv[r0:], 2e-2, True)
+    # dK, dV of early keys of the first two KV parts that a later Q part sees whole: every row of
+    # that Q part (and of the part's own diagonal Q part, from the key on) accumulates into them
+    # over the FULL-tile path; the oracle gets the GPU's merged O and LSE of those rows
+    past = [j for j, kv0 in enumerate(kv_offs) if any(q_offs[i] > kv0 for (i, b) in pairs if b == j)]
+    for j in past[:2]:
+        kv0 = kv_offs[j]
+        seers = [i for (i, b) in pairs if b == j]
+        for key in (0, 1, 127, 128, c // 2):
+            for hk in sorted({0, hkv - 1}):
+                hs = slice(hk * G, (hk + 1) * G)
+                sets = []
+                for i in seers:
+                    r0 = max(0, kv0 + key - q_offs[i])  # first row of Q part i that sees the key
+                    if r0 < c:
+                        sets.append((Q[i][r0:, hs], dO[i][r0:, hs], O[i][r0:, hs], L[i][hs, r0:],
+                                     q_offs[i] + r0))
+                gk, gv = key_oracle(sets, K[j][key:key + 1, hk:hk + 1], V[j][key:key + 1, hk:hk + 1],
+                                    kv0 + key)
+                check_close(f"dK kv{j} key{key} hk{hk}", f64(dK[j][key, hk]), gk, 2e-2, True)
+                check_close(f"dV kv{j} key{key} hk{hk}", f64(dV[j][key, hk]), gv, 2e-2, True)
     # every key of the share: each Q row's visible keys all lie in the share's KV parts, so the
     # sums over all KV parts match the sums over all Q parts
     dk_all = torch.cat(dK)

@@ -58,6 +58,22 @@ def normal(seed: int, tensor_id: int, shape, dtype: torch.dtype = torch.bfloat16
     return t if dtype == torch.float32 else t.to(dtype)
 
 
+def normal_device(seed: int, tensor_id: int, shape, dtype: torch.dtype = torch.bfloat16,
+                  device="cuda") -> torch.Tensor:
+    """Tensor of i.i.d. N(0,1) values of `shape` drawn on `device` by torch's seeded Philox
+    generator, 2^28 float32 values per draw (draw i seeded from (seed, tensor_id, i)), then cast
+    to `dtype`.  For tensors too large to draw on the host; the values differ from normal()'s."""
+    n = int(np.prod(shape)) if len(shape) else 1
+    out = torch.empty(n, dtype=dtype, device=device)
+    g = torch.Generator(device=device)
+    step = 1 << 28
+    for i, lo in enumerate(range(0, n, step)):
+        g.manual_seed(seed * 1000003 + tensor_id * 7919 + i)
+        hi = min(n, lo + step)
+        out[lo:hi] = torch.randn(hi - lo, generator=g, device=device).to(dtype)
+    return out.view(tuple(shape))
+
+
 TID_LOGITS, TID_LABELS = 40, 41
 
 

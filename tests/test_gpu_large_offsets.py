@@ -106,3 +106,107 @@ def test_offsets_beyond_32_bits(gpu):
     assert float(err_v[worst_v]) <= float(tol[worst_v]), ("sum dV", worst_v, float(err_v[worst_v]))
     del q, k, v, do, out, lse, dq, dk, dv, sk, sv, so, seg_id
     torch.cuda.empty_cache()
+
+
+def row_oracle(qrow, K, V, dorow, q_pos, k_pos):
+    """O, LSE, dQ of one query row [1, 1, d] against one key range [C, 1, d]."""
+    o, l = A.chunk_fwd(qrow, K, V, q_pos, k_pos, True, SCALE)
+    dq, _, _ = A.chunk_bwd(qrow, K, V, torch.from_numpy(o).to(BF), l, dorow, q_pos, k_pos, True,
+                           SCALE)
+    return o, l, dq
+
+
+def chunk_case(q, do, k_off, C, rows, check_keys, merge):
+    """Forward and backward of the 2^21 query rows at position 0 against a C-key chunk at
+    position k_off, through the C ABI; sampled rows against the oracle row by row.  With
+    check_keys, dK and dV of every key are checked element by element (only rows at or after
+    k_off see the chunk, so the oracle needs only those rows); otherwise by their sums over the
+    chunk.  With merge, a two-way LSE merge of 2^33 elements is checked too."""
+    dev = q.device
+    kc = inputs.normal_device(SEED, inputs.tid_chunk_k(0), (C, HKV, D), BF, dev)
+    vc = inputs.normal_device(SEED, inputs.tid_chunk_v(0), (C, HKV, D), BF, dev)
+    out, lse = B.bs_attn_chunk_fwd(q, kc, vc, 0, k_off, True, SCALE)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(out).all()) and not bool(torch.isnan(lse).any())
+    if k_off > 0:  # rows before the chunk see no key: O = 0, LSE = -inf
+        assert not bool(out[:k_off].any()) and bool(torch.isneginf(lse[:, :k_off]).all())
+
+    if merge:
+        # two partials that hold the same output with LSEs l and l + 1: O comes back bit for
+        # bit (a weighted mean of one bf16 value), the LSE is l + ln(1 + e), -inf stays -inf
+        parts = torch.stack([out, out])
+        lse_parts = torch.stack([lse, lse + 1.0])
+        mo, ml = B.bs_lse_merge(parts, lse_parts)
+        torch.cuda.synchronize()
+        assert torch.equal(mo, out), "merged O differs from its two identical partials"
+        want = lse.double() + math.log1p(math.e)
+        assert torch.equal(torch.isneginf(ml), torch.isneginf(lse)), "merged LSE: -inf pattern"
+        fin = torch.isfinite(lse)
+        lerr = float((ml.double()[fin] - want[fin]).abs().max()) if bool(fin.any()) else 0.0
+        assert lerr <= 1e-5, ("merged LSE", lerr)
+        del parts, lse_parts, mo, ml
+        torch.cuda.empty_cache()
+
+    dq_acc = torch.zeros(T, HQ, D, dtype=torch.float32, device=dev)
+    dq_acc, dk, dv = B.bs_attn_chunk_bwd(q, kc, vc, out, lse, do, 0, k_off, True, SCALE,
+                                         dq_accum=dq_acc)
+    dq = B.bs_dq_finalize(dq_acc, torch.empty_like(q))
+    torch.cuda.synchronize()
+    del dq_acc
+    for name, t in (("dQ", dq), ("dK", dk), ("dV", dv)):
+        assert bool(torch.isfinite(t).all()), f"{name}: non-finite values"
+    if k_off > 0:
+        assert not bool(dq[:k_off].any()), "dQ of rows that see no key"
+
+    rng = np.random.default_rng([SEED, 78, k_off])
+    for i in rows:
+        for h in sorted({0, HQ - 1, int(rng.integers(0, HQ))}):
+            hk = h // G
+            o, l, g = row_oracle(q[i:i + 1, h:h + 1].cpu(), kc[:, hk:hk + 1].cpu(),
+                                 vc[:, hk:hk + 1].cpu(), do[i:i + 1, h:h + 1].cpu(), i, k_off)
+            tag = f"row {i} h{h} (chunk at {k_off})"
+            check_close(f"O {tag}", f64(out[i, h]), o[0, 0], 2e-2, True)
+            check_lse(f"LSE {tag}", f64(lse[h, i:i + 1]), l[0], 1e-3)
+            check_close(f"dQ {tag}", f64(dq[i, h]), g[0, 0], 2e-2, True)
+
+    if check_keys:
+        # every key, all heads: the rows from k_off on, with the GPU's row-checked O and LSE
+        r0 = k_off
+        qb, dob, ob = (t[r0:].cpu() for t in (q, do, out))
+        _, gk, gv = A.chunk_bwd(qb, kc.cpu(), vc.cpu(), ob, lse[:, r0:].cpu(), dob, r0, k_off, True,
+                                SCALE)
+        check_close(f"dK (chunk at {k_off})", f64(dk), gk, 2e-2, True)
+        check_close(f"dV (chunk at {k_off})", f64(dv), gv, 2e-2, True)
+    else:
+        # sum_j dK_j = 0 and sum_j dV_j = the group's sum of dO (this chunk is the only step)
+        so = torch.zeros(HKV, D, dtype=torch.float64, device=dev)
+        for s0 in range(0, T, 1 << 18):
+            so += do[s0:s0 + (1 << 18)].double().reshape(-1, HKV, G, D).sum(dim=(0, 2))
+        sk, sv = dk.double().sum(dim=0), dv.double().sum(dim=0)
+        tol = 0.02 * math.sqrt(C * G) + 1e-3 * float(so.abs().max())
+        assert float(sk.abs().max()) <= tol, ("sum dK", float(sk.abs().max()), tol)
+        assert float((sv - so).abs().max()) <= tol, ("sum dV", float((sv - so).abs().max()), tol)
+    del kc, vc, out, lse, dq, dk, dv
+    torch.cuda.empty_cache()
+
+
+def test_chunk_merge_finalize_offsets_beyond_32_bits(gpu):
+    """The context-parallel path at the same sizes: 2^21 query rows (2^32 elements per
+    Q-sized tensor, a float32 dQ accumulator of 16 GiB and its finalize) against a 256-key
+    chunk
+      * at the end of the sequence: only the last rows (Q offsets near 2^32) see it, the rest
+        get O = 0 and LSE = -inf; a two-way LSE merge of 2^33 elements; dK and dV of every key
+        element by element;
+      * at the start: every row sees it; sampled rows where Q's offset crosses 2^31 and
+        3 * 2^30; dK and dV by their sums (each key sums 2^22 bf16 products of P and dS,
+        whose rounding alone is of the order of the 2e-2 bound there)."""
+    C = 256
+    dev = torch.device("cuda")
+    q = inputs.normal_device(SEED, inputs.TID_Q, (T, HQ, D), BF, dev)
+    do = inputs.normal_device(SEED, inputs.TID_DO, (T, HQ, D), BF, dev)
+    row_per_elem = HQ * D
+    chunk_case(q, do, T - C, C, [0, T - C - 1, T - C, T - C + 1, T - 2, T - 1], True, True)
+    chunk_case(q, do, 0, C, [0, 1, C - 1, C, (1 << 31) // row_per_elem,
+                             (3 << 30) // row_per_elem, T - 1], False, False)
+    del q, do
+    torch.cuda.empty_cache()

@@ -23,7 +23,7 @@ template <> __device__ __forceinline__ float from_f<float>(float x) { return x; 
 // sets (the steps of a context-parallel ring):
 //   LSE = m + log(sum_c exp(LSE_c - m)),   O = sum_c exp(LSE_c - LSE) O_c,
 // m = max_c LSE_c; partials at -inf weigh 0; all -inf gives O = 0, LSE = -inf.
-template <typename T, int D>
+template <typename T, int D, int U>
 __global__ __launch_bounds__(256) void lse_merge_kernel(const T* __restrict__ parts,
                                                         const float* __restrict__ lse_parts,
                                                         int32_t n, int64_t rows, int32_t hq,
@@ -39,22 +39,44 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const T* __restrict__ pa
   const int h = row % hq;
   const float* lp = lse_parts + (int64_t)h * total_q + t;
   const int64_t lstride = (int64_t)hq * total_q;
-  float m = -INFINITY;
-  for (int c = 0; c < n; ++c) m = fmaxf(m, lp[c * lstride]);
+  const int64_t pstride = rows * D;
+  const T* src = parts + row * D + part * Vec<T>::N;
   float acc[Vec<T>::N];
 #pragma unroll
   for (int i = 0; i < Vec<T>::N; ++i) acc[i] = 0.f;
-  float wsum = 0.f;
-  if (m != -INFINITY) {
-    const int64_t pstride = rows * D;
-    const T* src = parts + row * D + part * Vec<T>::N;
-    for (int c = 0; c < n; ++c) {
-      const float wgt = expf(lp[c * lstride] - m);  // exp(-inf) = 0
-      wsum += wgt;
-      const V x = *reinterpret_cast<const V*>(src + c * pstride);
+  float m = -INFINITY, wsum = 0.f;
+  // partials in groups of U: every load of a group is issued before any of it is used, so
+  // that each lane keeps U row reads in flight (one at a time is latency-bound); the sum is
+  // rescaled when a group raises the running maximum
+  for (int c0 = 0; c0 < n; c0 += U) {
+    float l[U];
+    V x[U];
 #pragma unroll
-      for (int i = 0; i < Vec<T>::N; ++i) acc[i] += wgt * to_f(x[i]);
+    for (int u = 0; u < U; ++u) {
+      if (c0 + u < n) {
+        l[u] = lp[(c0 + u) * lstride];
+        x[u] = __builtin_nontemporal_load(reinterpret_cast<const V*>(src + (c0 + u) * pstride));
+      } else {
+        l[u] = -INFINITY;
+        x[u] = V{};
+      }
     }
+    float mg = m;
+#pragma unroll
+    for (int u = 0; u < U; ++u) mg = fmaxf(mg, l[u]);
+    if (mg == -INFINITY) continue;
+    const float r = expf(m - mg);  // 0 while nothing was added (m = -inf)
+    wsum *= r;
+#pragma unroll
+    for (int i = 0; i < Vec<T>::N; ++i) acc[i] *= r;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float wgt = expf(l[u] - mg);  // exp(-inf) = 0
+      wsum += wgt;
+#pragma unroll
+      for (int i = 0; i < Vec<T>::N; ++i) acc[i] += wgt * to_f(x[u][i]);
+    }
+    m = mg;
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   V y;
@@ -124,16 +146,23 @@ hipError_t launch_lse_merge(const bs_dims& dims, const void* out_parts, const fl
   if (rows == 0) return hipSuccess;
   const int vec = dims.dtype == BS_BF16 ? 8 : 4;
   const unsigned grid = blocks_for(rows * (dims.head_dim / vec));
-#define BS_MERGE(T, D)                                                                        \
-  hipLaunchKernelGGL((lse_merge_kernel<T, D>), dim3(grid), dim3(256), 0, stream,             \
+#define BS_MERGE_U(T, D, U)                                                                   \
+  hipLaunchKernelGGL((lse_merge_kernel<T, D, U>), dim3(grid), dim3(256), 0, stream,          \
                      static_cast<const T*>(out_parts), lse_parts, n, rows, dims.hq,           \
                      dims.total_q, static_cast<T*>(out), lse)
+#define BS_MERGE(T, D)                                                                        \
+  do {                                                                                        \
+    if (n <= 2) BS_MERGE_U(T, D, 2);                                                          \
+    else if (n <= 4) BS_MERGE_U(T, D, 4);                                                     \
+    else BS_MERGE_U(T, D, 8);                                                                 \
+  } while (0)
   if (dims.dtype == BS_BF16) {
     if (dims.head_dim == 128) BS_MERGE(bf16, 128); else BS_MERGE(bf16, 64);
   } else {
     if (dims.head_dim == 128) BS_MERGE(float, 128); else BS_MERGE(float, 64);
   }
 #undef BS_MERGE
+#undef BS_MERGE_U
   return hipGetLastError();
 }
 

@@ -21,6 +21,7 @@
 //   plan_count : validate cu_seqlens, per-segment tile counts, exclusive scan
 //   plan_rank  : one thread per segment: its first slot in the ordered list
 //   plan_emit  : one thread per list entry, fills its fields at its slot
+// or, for up to 1024 segments, the same three steps in one workgroup (plan_fused).
 #include "common.hpp"
 
 namespace bs {
@@ -59,14 +60,15 @@ __device__ __forceinline__ Seg load_seg(const int32_t* cu_q, const int32_t* cu_k
   return s;
 }
 
-// Validates cu_seqlens, computes items per segment and their exclusive prefix.
-__global__ __launch_bounds__(kCountThreads) void plan_count(
-    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int32_t num_seqs,
-    int64_t total_q, int64_t total_k, int32_t max_seqlen, int kind, int tile_a,
-    WsHeader* __restrict__ hdr, int32_t* __restrict__ seg_off) {
-  __shared__ int32_t scan[kCountThreads];
-  __shared__ int32_t carry;
-  __shared__ int32_t status;
+// Validates cu_seqlens, computes items per segment and their exclusive prefix into seg_off
+// (nseg + 1 entries), and the status word and item count into the header.  One workgroup
+// of kCountThreads threads; scan, carry and status are its LDS.
+__device__ __forceinline__ void count_body(const int32_t* __restrict__ cu_q,
+                                           const int32_t* __restrict__ cu_k, int32_t num_seqs,
+                                           int64_t total_q, int64_t total_k, int32_t max_seqlen,
+                                           int kind, int tile_a, WsHeader* __restrict__ hdr,
+                                           int32_t* seg_off, int32_t* scan, int32_t& carry,
+                                           int32_t& status) {
   const int t = threadIdx.x;
   if (t == 0) { carry = 0; status = 0; }
   __syncthreads();
@@ -107,15 +109,23 @@ __global__ __launch_bounds__(kCountThreads) void plan_count(
   }
 }
 
-__global__ __launch_bounds__(256) void plan_emit(
-    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k,
+__global__ __launch_bounds__(kCountThreads) void plan_count(
+    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int32_t num_seqs,
+    int64_t total_q, int64_t total_k, int32_t max_seqlen, int kind, int tile_a,
+    WsHeader* __restrict__ hdr, int32_t* __restrict__ seg_off) {
+  __shared__ int32_t scan[kCountThreads];
+  __shared__ int32_t carry;
+  __shared__ int32_t status;
+  count_body(cu_q, cu_k, num_seqs, total_q, total_k, max_seqlen, kind, tile_a, hdr, seg_off, scan,
+             carry, status);
+}
+
+// List entry i (0 <= i < the item count): its segment, tile and counts, written at its slot.
+__device__ __forceinline__ void emit_body(
+    int64_t i, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k,
     const int64_t* __restrict__ q_pos, const int64_t* __restrict__ k_pos, int32_t num_seqs,
     int64_t total_q, int64_t total_k, int32_t diag_chunk, int causal, int kind, int tile_a,
-    int tile_b, int64_t max_items, const WsHeader* __restrict__ hdr,
-    const int32_t* __restrict__ seg_off, const int32_t* __restrict__ seg_dst,
-    WorkItem* __restrict__ items) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= max_items || i >= hdr->n_items) return;
+    int tile_b, const int32_t* seg_off, const int32_t* seg_dst, WorkItem* __restrict__ items) {
   const int32_t nseg = cu_q == nullptr ? 1 : num_seqs;
   // segment b with seg_off[b] <= i < seg_off[b+1] (skipping empty segments)
   int32_t lo = 0, hi = nseg - 1;
@@ -186,6 +196,19 @@ __global__ __launch_bounds__(256) void plan_emit(
   items[seg_dst[b] + (kind == kPlanFwd ? cnt - 1 - tile : tile)] = w;
 }
 
+__global__ __launch_bounds__(256) void plan_emit(
+    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k,
+    const int64_t* __restrict__ q_pos, const int64_t* __restrict__ k_pos, int32_t num_seqs,
+    int64_t total_q, int64_t total_k, int32_t diag_chunk, int causal, int kind, int tile_a,
+    int tile_b, int64_t max_items, const WsHeader* __restrict__ hdr,
+    const int32_t* __restrict__ seg_off, const int32_t* __restrict__ seg_dst,
+    WorkItem* __restrict__ items) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= max_items || i >= hdr->n_items) return;
+  emit_body(i, cu_q, cu_k, q_pos, k_pos, num_seqs, total_q, total_k, diag_chunk, causal, kind,
+            tile_a, tile_b, seg_off, seg_dst, items);
+}
+
 // First slot of each segment in the ordered list: the items of every segment that
 // comes before it (larger len_q + len_k, or equal size and a lower index).
 constexpr int kRankChunk = 1024;
@@ -222,6 +245,48 @@ __global__ __launch_bounds__(256) void plan_rank(const int32_t* __restrict__ cu_
   if (b < nseg) seg_dst[b] = (int32_t)dst;
 }
 
+// All three steps in one workgroup, for up to kCountThreads segments (one thread per segment
+// in the ranking): the per-segment offsets and first slots stay in LDS, and the list
+// entries are filled in a loop over the workgroup.  Same list as the three kernels.
+__global__ __launch_bounds__(kCountThreads) void plan_fused(
+    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k,
+    const int64_t* __restrict__ q_pos, const int64_t* __restrict__ k_pos, int32_t num_seqs,
+    int64_t total_q, int64_t total_k, int32_t max_seqlen, int32_t diag_chunk, int causal,
+    int kind, int tile_a, int tile_b, int64_t max_items, WsHeader* __restrict__ hdr,
+    WorkItem* __restrict__ items) {
+  __shared__ int32_t scan[kCountThreads];
+  __shared__ int32_t soff[kCountThreads + 1];
+  __shared__ int32_t sdst[kCountThreads];
+  __shared__ int64_t ssz[kCountThreads];
+  __shared__ int32_t carry;
+  __shared__ int32_t status;
+  count_body(cu_q, cu_k, num_seqs, total_q, total_k, max_seqlen, kind, tile_a, hdr, soff, scan,
+             carry, status);
+  __syncthreads();
+  if (status != 0 || max_items == 0) return;  // uniform: the list is empty
+  const int32_t nseg = cu_q == nullptr ? 1 : num_seqs;
+  const int t = threadIdx.x;
+  // first slot of segment t: the items of every segment that comes before it (larger
+  // len_q + len_k, or equal size and a lower index)
+  const int64_t mine =
+      (cu_q != nullptr && t < nseg) ? ((int64_t)cu_q[t + 1] - cu_q[t]) + ((int64_t)cu_k[t + 1] - cu_k[t]) : 0;
+  ssz[t] = mine;
+  __syncthreads();
+  if (t < nseg) {
+    int32_t dst = 0;
+    for (int32_t j = 0; j < nseg; ++j) {
+      const bool before = ssz[j] > mine || (ssz[j] == mine && j < t);
+      dst += before ? soff[j + 1] - soff[j] : 0;
+    }
+    sdst[t] = dst;
+  }
+  __syncthreads();
+  const int64_t n = carry < max_items ? carry : max_items;
+  for (int64_t i = t; i < n; i += kCountThreads)
+    emit_body(i, cu_q, cu_k, q_pos, k_pos, num_seqs, total_q, total_k, diag_chunk, causal, kind,
+              tile_a, tile_b, soff, sdst, items);
+}
+
 }  // namespace
 
 hipError_t launch_plan(PlanKind kind, const int32_t* cu_q, const int32_t* cu_k,
@@ -234,6 +299,13 @@ hipError_t launch_plan(PlanKind kind, const int32_t* cu_q, const int32_t* cu_k,
   int32_t* seg_off = reinterpret_cast<int32_t*>(base + L.seg_off);
   int32_t* seg_dst = reinterpret_cast<int32_t*>(base + L.seg_dst);
   WorkItem* sorted = reinterpret_cast<WorkItem*>(base + L.sorted);
+  const int32_t nsegs = cu_q == nullptr ? 1 : num_seqs;
+  if (nsegs <= kCountThreads) {
+    hipLaunchKernelGGL(plan_fused, dim3(1), dim3(kCountThreads), 0, stream, cu_q, cu_k, q_pos,
+                       k_pos, num_seqs, total_q, total_k, max_seqlen, diag_chunk, causal, (int)kind,
+                       tile_a, tile_b, max_items, hdr, sorted);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(plan_count, dim3(1), dim3(kCountThreads), 0, stream, cu_q, cu_k, num_seqs,
                      total_q, total_k, max_seqlen, (int)kind, tile_a, hdr, seg_off);
   if (max_items > 0) {

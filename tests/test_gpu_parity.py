@@ -246,7 +246,11 @@ def test_lse_merge_with_neg_inf_partials(gpu, dtype):
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_plan_export_bit_exact(gpu, dtype):
     rng = np.random.default_rng(13)
-    cases = [RAGGED, [0, 0, 5], [32768], list(rng.integers(0, 900, size=40))]
+    # up to 1024 segments the planner runs as one workgroup, beyond that as three kernels:
+    # 1024, 1025 and 1500 segments (many equal sizes: the index breaks the ties) cover both
+    cases = [RAGGED, [0, 0, 5], [32768], list(rng.integers(0, 900, size=40)),
+             list(rng.integers(0, 300, size=1024)), list(rng.integers(0, 300, size=1025)),
+             list(rng.integers(0, 300, size=1500))]
     for lens in cases:
         lens = [int(x) for x in lens]
         cu = torch.from_numpy(inputs.cu_seqlens(lens)).cuda()

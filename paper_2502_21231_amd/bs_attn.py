@@ -477,7 +477,7 @@ def bs_softmax_xent(logits, labels, ignore_index: int = -100, grad_scale: float 
 
 
 def bs_read_device_status(workspace) -> int:
-    """Synchronises and returns BS_OK or raises BsError with the device planner's verdict."""
+    """Synchronises and returns BS_OK or raises BsError with the device planner's status."""
     _check(load_library().bs_read_device_status(_ptr(workspace), _stream(workspace.device)))
     return BS_OK
 

@@ -221,7 +221,7 @@ def time_steps(step, args, dev, flops_fwd, flops_bwd):
 
 
 # The CPU oracle runs on a bounded sample of each workload (about 10-30 s of float64 work on
-# the GPU machine's 16 host cores), so that a default benchmark run stays within minutes; the
+# the benchmark host's 16 cores), so that a default benchmark run stays within minutes; the
 # full-problem time is extrapolated from it and labelled as such.  The oracle computes every
 # (row, key) score of a segment or chunk and masks it, so its time is proportional to
 # rows x keys x query heads (not to the visible pairs): that is the extrapolation factor.

@@ -20,7 +20,11 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libbs_attn.so")
 
-SOURCES = ["plan.hip", "fwd_bf16.hip", "bwd_bf16.hip", "f32.hip", "rowwise.hip", "xent.hip", "capi.hip"]
+SOURCES = ["plan.hip", "fwd_bf16.hip", "dq_bf16.hip", "dkdv_bf16.hip", "f32.hip", "rowwise.hip",
+           "xent.hip", "capi.hip"]
+# per-source additions: the dQ kernel's loop schedules faster under the backend's max-ILP
+# strategy (the forward's and dK/dV's do not)
+SOURCE_FLAGS = {"dq_bf16.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]}
 # host-only planners (no GPU code): a library of their own, built with the host compiler
 HDP_SOURCE = "hdp.cpp"
 HDP_LIB = os.path.join(PKG, "libbs_hdp.so")
@@ -82,7 +86,7 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     for src in SOURCES:
         obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
-        cmds.append([cc, *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([cc, *CFLAGS, *SOURCE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj])
     jobs = jobs or min(len(cmds), max(1, min(8, os.cpu_count() or 1)))
     with ThreadPoolExecutor(jobs) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))

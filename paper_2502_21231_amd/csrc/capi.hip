@@ -70,14 +70,28 @@ hipEvent_t take_event() {
   return e;
 }
 
-// Records an event pair around the launches made during its lifetime.
+void give_back(hipEvent_t e) {
+  if (e == nullptr) return;
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> g(P.mu);
+  P.spare.push_back(e);
+}
+
+// Records an event pair around the launches made during its lifetime (none when an event
+// cannot be had: the one that was is returned to the pool).
 class ProfScope {
  public:
   ProfScope(int kind, hipStream_t s) : kind_(kind), s_(s) {
     if (!prof().on.load(std::memory_order_relaxed)) return;
     a_ = take_event();
     b_ = take_event();
-    if (a_ && b_) hipEventRecord(a_, s_);
+    if (a_ && b_) {
+      hipEventRecord(a_, s_);
+    } else {
+      give_back(a_);
+      give_back(b_);
+      a_ = b_ = nullptr;
+    }
   }
   ~ProfScope() {
     if (!a_ || !b_) return;

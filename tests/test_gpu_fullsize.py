@@ -131,6 +131,15 @@ def test_packed_7b_32k_lognormal_seed0(gpu):
     varlen_fullsize(inputs.lognormal_packed_lengths(0), 32, 32, 0)
 
 
+@pytest.mark.parametrize("seed", [1, 2, 3, 4])
+def test_packed_7b_32k_lognormal_other_seeds(gpu, seed):
+    """The same workload for the other seeds the benchmark reports (longest segments 4,549,
+    19,849, 29,532 and 15,866 tokens: early keys there accumulate over up to 29,532 rows)."""
+    lens = inputs.lognormal_packed_lengths(seed)
+    print(f"seed {seed}: {len(lens)} segments, longest {max(lens)}", flush=True)
+    varlen_fullsize(lens, 32, 32, seed)
+
+
 def test_gqa_70b_131k_mixed_seed0(gpu):
     """131072 tokens, 64/8 heads, one 60642-token segment among 33 shorts."""
     varlen_fullsize(inputs.mixed_long_short_lengths(0), 64, 8, 0)

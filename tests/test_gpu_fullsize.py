@@ -145,6 +145,11 @@ def test_gqa_70b_131k_mixed_seed0(gpu):
     varlen_fullsize(inputs.mixed_long_short_lengths(0), 64, 8, 0)
 
 
+def test_gqa_70b_131k_mixed_two_long_seed1(gpu):
+    """The same mix with two long segments (48,273 and 33,218 tokens) among 22 shorts."""
+    varlen_fullsize(inputs.mixed_long_short_lengths(1), 64, 8, 1)
+
+
 def chunk_share(hq, hkv, q_offs, kv_offs, pairs, seed, c=32768, ring=False):
     """A context-parallel share: per-step chunk forward, LSE merge, per-step chunk backward with
     dQ (and, for KV parts seen by several Q parts, dK/dV) accumulated in float32.  With ring=True

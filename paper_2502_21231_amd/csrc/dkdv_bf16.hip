@@ -21,7 +21,14 @@
 //   wave's products; the P hand-off is one LDS-only barrier per query tile,
 //   at which the copy of the next tile stays in flight.  dK, dV of every key are
 //   accumulated over all query heads of the KV group and all visible query
-//   tiles (MASKED diagonal tiles first) and written once.
+//   tiles and written once.  With one query head per KV head the query tiles
+//   are walked from the diagonal (MASKED tiles first) to the end of the segment.
+//   With a group of several, from the last tile of the segment down to the
+//   diagonal, the heads of the group innermost: the workgroups of one segment's
+//   key tiles that run together on an XCD (one KV head per XCD) then read the same
+//   query tile of the same head at about the same time, once from HBM into that
+//   XCD's L2; walked upwards, each starts at its own diagonal, and its head
+//   changes at its own time.
 //   Query rows past the segment use LSE = +inf (P = 0), rows whose LSE is
 //   -inf (no visible key) also get P = 0.
 //
@@ -37,7 +44,7 @@
 namespace bs {
 namespace {
 
-template <int D>
+template <int D, bool kGroupOrder>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void dkdv_bf16_kernel(const BwdParams p) {
   constexpr int BM = kBwdBM, BN = kBwdBN;
@@ -92,6 +99,17 @@ void dkdv_bf16_kernel(const BwdParams p) {
   const int qt_first = it.n0, n_masked = it.n1, n_vis = it.n2;
   const int diag = it.diag;
   const int n_iter = n_vis * p.group;
+  // step i: query tile j (relative to qt_first) of query head hg of the group
+  auto tile_of = [&](int i, int& hg, int& j) {
+    if constexpr (kGroupOrder) {  // last tile first, heads innermost
+      const int s = i / p.group;
+      hg = i - s * p.group;
+      j = n_vis - 1 - s;
+    } else {                      // diagonal first, heads outermost
+      hg = i / n_vis;
+      j = i - hg * n_vis;
+    }
+  };
 
   // All eight waves copy query tile i (head, rows) into QDd; the first S wave fetches its
   // LSE rows, the second its D rows, and the S waves store them at the end of the step,
@@ -101,7 +119,8 @@ void dkdv_bf16_kernel(const BwdParams p) {
   float row_r = 0.f;   // raw LSE / D value of one row (converted when stored)
   bool row_ok = false;  // the row lies inside the segment
   auto copy_tile = [&](int i, bf16* QDd) {
-    const int hg = i / n_vis, j = i - hg * n_vis;
+    int hg, j;
+    tile_of(i, hg, j);
     const int h = hk * p.group + hg;
     const int q_rel0 = (qt_first + j) * BM;
     const int64_t q_glob0 = (int64_t)it.b_start + q_rel0;
@@ -137,7 +156,8 @@ void dkdv_bf16_kernel(const BwdParams p) {
   // one query tile: consume (QDb, Rb) while tile i+1 is copied into (QDn, Rn),
   // which were last read one tile earlier, before the barrier that ended it
   auto step = [&](int i, const bf16* QDb, const float* Rb, bf16* QDn, float* Rn) {
-    const int hg = i / n_vis, j = i - hg * n_vis;
+    int hg, j;
+    tile_of(i, hg, j);
     const int q_rel0 = (qt_first + j) * BM;
     const bool masked = j < n_masked;
     const bf16* A1 = QDb + base1;
@@ -296,10 +316,18 @@ hipError_t launch_dkdv_bf16(const bs_dims& dims, const void* q, const void* k, c
     p.dv = static_cast<bf16*>(dv);
   }
   const dim3 grid((unsigned)(L.max_items * dims.hkv));
-  if (dims.head_dim == 128)
-    hipLaunchKernelGGL(dkdv_bf16_kernel<128>, grid, dim3(512), 0, stream, p);
-  else
-    hipLaunchKernelGGL(dkdv_bf16_kernel<64>, grid, dim3(512), 0, stream, p);
+  const bool group_order = p.group > 1;
+  if (dims.head_dim == 128) {
+    if (group_order)
+      hipLaunchKernelGGL((dkdv_bf16_kernel<128, true>), grid, dim3(512), 0, stream, p);
+    else
+      hipLaunchKernelGGL((dkdv_bf16_kernel<128, false>), grid, dim3(512), 0, stream, p);
+  } else {
+    if (group_order)
+      hipLaunchKernelGGL((dkdv_bf16_kernel<64, true>), grid, dim3(512), 0, stream, p);
+    else
+      hipLaunchKernelGGL((dkdv_bf16_kernel<64, false>), grid, dim3(512), 0, stream, p);
+  }
   return hipGetLastError();
 }
 

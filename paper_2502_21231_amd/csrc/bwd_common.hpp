@@ -30,10 +30,6 @@ struct BwdParams {
   float scale, scale_log2;
 };
 
-__device__ __forceinline__ int spread_head(int slot, int n) {
-  return (n & 7) == 0 ? (slot & 7) * (n >> 3) + (slot >> 3) : slot;
-}
-
 inline BwdParams make_params(const bs_dims& dims, const void* q, const void* k, const void* v,
                       const void* dout, const float* lse, const float* dvec, int causal,
                       float scale, const void* ws, const WsLayout& L) {

@@ -26,8 +26,10 @@ constexpr int kDiagClamp = 1 << 30;
 // Backward (key tile):   seg, tile=ktile, a_start=k_start, a_rows=k_rows,
 //                        b_start=q_start, b_len=q_len, n0=qt_first, n1=n_masked,
 //                        n2=n_vis, diag.
+// Both: run0 = list slot of the first item of the segment, nrun = the segment's item
+// count (the items of a segment are contiguous in the list).
 struct WorkItem {
-  int32_t seg, tile, a_start, a_rows, b_start, b_len, n0, n1, n2, diag, pad0, pad1;
+  int32_t seg, tile, a_start, a_rows, b_start, b_len, n0, n1, n2, diag, run0, nrun;
 };
 static_assert(sizeof(WorkItem) == 48, "work item is 12 int32");
 
@@ -48,6 +50,48 @@ struct WsHeader {
   int32_t n_items;
   int32_t pad[62];
 };
+
+// A segment streams this many rows (b_len) or more: its run is walked one head at a time.
+constexpr int kHeadMajorRows = 16384;
+
+// Work item and head of this workgroup in a grid of n_items * n_heads blocks; false when it
+// has none.  Blocks are dealt to the 8 XCDs round-robin (block b runs on XCD b % 8), so with
+// n_heads a multiple of 8 each XCD owns the hx = n_heads / 8 heads x*hx .. x*hx+hx-1 and walks
+// the list segment by segment.  Inside a segment's run its heads are interleaved item by
+// item, except where the segment streams at least kHeadMajorRows rows and the XCD's heads
+// read more than one stream (hx > heads_per_stream: heads that share a KV head share its
+// K/V stream): there the XCD walks one head's items at a time, so that the workgroups
+// resident on it read one stream, not hx / heads_per_stream, and each tile of it comes into
+// the XCD's L2 that many times less often.
+__device__ __forceinline__ bool block_work(const WsHeader* __restrict__ hdr,
+                                           const WorkItem* __restrict__ items, int n_heads,
+                                           int heads_per_stream, WorkItem& it, int& head) {
+  const int b = blockIdx.x;
+  const int n_items = hdr->n_items;
+  if ((n_heads & 7) != 0) {
+    const int i = b / n_heads;
+    if (i >= n_items) return false;
+    it = items[i];
+    head = b - i * n_heads;
+    return true;
+  }
+  const int hx = n_heads >> 3, jb = b >> 3;
+  const int g = jb / hx;
+  if (g >= n_items) return false;
+  const WorkItem gi = items[g];
+  const int r = jb - gi.run0 * hx;  // 0 <= r < nrun * hx: this block's place in the run
+  int i, hl;
+  if (hx > heads_per_stream && gi.b_len >= kHeadMajorRows) {
+    hl = r / gi.nrun;
+    i = gi.run0 + (r - hl * gi.nrun);
+  } else {
+    i = g;
+    hl = r - (g - gi.run0) * hx;
+  }
+  it = i == g ? gi : items[i];
+  head = (b & 7) * hx + hl;
+  return true;
+}
 
 struct WsLayout {
   size_t seg_off;     // int32[num_seqs + 1]

@@ -65,10 +65,9 @@ void dkdv_bf16_kernel(const BwdParams p) {
   // bf16 P handed from the S wave to the dP wave of each key block: [block][step][lane]
   __shared__ __attribute__((aligned(16))) bf16x8 Ps[4 * QS * 64];
 
-  const int item_idx = blockIdx.x / p.hkv;
-  if (item_idx >= p.hdr->n_items) return;
-  const WorkItem it = p.items[item_idx];
-  const int hk = spread_head(blockIdx.x % p.hkv, p.hkv);
+  WorkItem it;
+  int hk;  // KV head; each reads the Q/dO stream of its own query heads
+  if (!block_work(p.hdr, p.items, p.hkv, 1, it, hk)) return;
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, c = lane & 31, hh = lane >> 5;

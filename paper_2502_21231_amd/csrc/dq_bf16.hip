@@ -37,10 +37,9 @@ void dq_bf16_kernel(const BwdParams p) {
   __shared__ __attribute__((aligned(16))) bf16 V0[TILE];
   __shared__ __attribute__((aligned(16))) bf16 V1[TILE];
 
-  const int item_idx = blockIdx.x / p.hq;
-  if (item_idx >= p.hdr->n_items) return;
-  const WorkItem it = p.items[item_idx];
-  const int h = spread_head(blockIdx.x % p.hq, p.hq);
+  WorkItem it;
+  int h;  // query head; the query heads of one KV group share its K/V stream
+  if (!block_work(p.hdr, p.items, p.hq, p.group, it, h)) return;
   const int hk = h / p.group;
 
   const int tid = threadIdx.x;

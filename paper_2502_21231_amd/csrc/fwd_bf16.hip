@@ -57,13 +57,6 @@ struct FwdParams {
 
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
 
-// Query head handled by a block: heads are spread so that all blocks of one
-// head (and of one KV group) fall on the same XCD when hq is a multiple of 8
-// (blocks are dealt to the 8 XCDs round-robin by block index).
-__device__ __forceinline__ int head_of(int slot, int hq) {
-  return (hq & 7) == 0 ? (slot & 7) * (hq >> 3) + (slot >> 3) : slot;
-}
-
 template <int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void fwd_bf16_kernel(const FwdParams p) {
@@ -80,10 +73,9 @@ void fwd_bf16_kernel(const FwdParams p) {
   __shared__ __attribute__((aligned(16))) bf16 V0[TILE];
   __shared__ __attribute__((aligned(16))) bf16 V1[TILE];
 
-  const int item_idx = blockIdx.x / p.hq;
-  if (item_idx >= p.hdr->n_items) return;
-  const WorkItem it = p.items[item_idx];
-  const int h = head_of(blockIdx.x % p.hq, p.hq);
+  WorkItem it;
+  int h;  // query head; the query heads of one KV group share its K/V stream
+  if (!block_work(p.hdr, p.items, p.hq, p.group, it, h)) return;
   const int hk = h / p.group;
 
   const int tid = threadIdx.x;

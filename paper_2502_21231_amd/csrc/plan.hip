@@ -138,7 +138,7 @@ __device__ __forceinline__ void emit_body(
   const int64_t tile = i - seg_off[b];
   const int64_t diag = s.diag;
   WorkItem w;
-  w.seg = b; w.tile = (int32_t)tile; w.diag = s.diag; w.pad0 = 0; w.pad1 = 0;
+  w.seg = b; w.tile = (int32_t)tile; w.diag = s.diag; w.run0 = seg_dst[b]; w.nrun = (int32_t)(seg_off[b + 1] - seg_off[b]);
   if (kind == kPlanFwd) {
     const int64_t BM = tile_a, BN = tile_b;
     const int64_t q_first = tile * BM;

@@ -150,6 +150,13 @@ def test_gqa_70b_131k_mixed_two_long_seed1(gpu):
     varlen_fullsize(inputs.mixed_long_short_lengths(1), 64, 8, 1)
 
 
+def test_gqa_two_kv_groups_per_xcd_long_and_short_segments(gpu):
+    """64/16 heads: each XCD holds two KV groups (8 query heads, 2 KV heads), so a segment of
+    16,384 rows or more is walked one head at a time in all three kernels, and the shorter ones
+    head by head interleaved; one 20,480-token segment among shorter ones (one of 128)."""
+    varlen_fullsize([3000, 20480, 700, 9000, 128], 64, 16, 7)
+
+
 def chunk_share(hq, hkv, q_offs, kv_offs, pairs, seed, c=32768, ring=False):
     """A context-parallel share: per-step chunk forward, LSE merge, per-step chunk backward with
     dQ (and, for KV parts seen by several Q parts, dK/dV) accumulated in float32.  With ring=True

@@ -76,6 +76,14 @@ def test_empty_segments_and_single_tokens(gpu):
     run_varlen([0, 1, 0, 1, 130, 0], 2, 2, 64, torch.bfloat16, seed=6)
 
 
+@pytest.mark.parametrize("hq,hkv", [(16, 16), (16, 4), (24, 8)])
+def test_several_heads_per_xcd(gpu, hq, hkv):
+    """Head counts that are multiples of 8: each of the 8 XCDs owns hq/8 query heads (hkv/8 KV
+    heads in dK/dV, when that divides), interleaved item by item along each segment's run of
+    the work list; ragged segments, an empty one and a single token."""
+    run_varlen([300, 1, 770, 0, 64, 129], hq, hkv, 128, torch.bfloat16, seed=8)
+
+
 def test_varlen_q_shorter_than_k_bottom_right(gpu):
     """len_q != len_k: the causal diagonal is aligned bottom-right."""
     lq, lk = [10, 70, 3], [50, 70, 130]

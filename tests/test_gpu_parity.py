@@ -76,6 +76,38 @@ def test_empty_segments_and_single_tokens(gpu):
     run_varlen([0, 1, 0, 1, 130, 0], 2, 2, 64, torch.bfloat16, seed=6)
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_empty_batches(gpu, dtype):
+    """No tokens at all: no segments, and three empty ones (forward and backward return empty
+    outputs without error)."""
+    for lens in ([], [0, 0, 0]):
+        run_varlen(lens, 4, 2, 64, dtype, seed=9)
+
+
+@pytest.mark.parametrize("tq,tk", [(0, 70), (50, 0)])
+def test_chunk_without_queries_or_keys(gpu, tq, tk):
+    """A chunk with no query rows (dK = dV = 0) or no keys (O = 0, LSE = -inf, dQ unchanged)."""
+    hq, hkv, d, dtype = 4, 2, 128, torch.bfloat16
+    q, k, v, do = make_qkv(10, tq, tk, hq, hkv, d, dtype)
+    qg, kg, vg, dog = to_gpu(q, k, v, do)
+    scale = scale_for(d)
+    out, lse = B.bs_attn_chunk_fwd(qg, kg, vg, 500, 400, True, scale)
+    o_ref, lse_ref = A.chunk_fwd(q, k, v, 500, 400, True, scale)
+    check_close("O", f64(out), o_ref, TOL[dtype]["o"], True)
+    check_lse("LSE", f64(lse), lse_ref, TOL[dtype]["lse"])
+    o_in = torch.from_numpy(o_ref).to(dtype)
+    acc = torch.full((tq, hq, d), 0.5, dtype=torch.float32, device="cuda")
+    # dK, dV start as 7 so that the kernel has to write the zeros of a key nobody sees
+    dk0 = torch.full(k.shape, 7.0, dtype=dtype, device="cuda")
+    dv0 = torch.full(v.shape, 7.0, dtype=dtype, device="cuda")
+    acc, dk, dv = B.bs_attn_chunk_bwd(qg, kg, vg, o_in.cuda(), torch.from_numpy(lse_ref).float().cuda(),
+                                      dog, 500, 400, True, scale, dq_accum=acc, dk=dk0, dv=dv0)
+    g = A.chunk_bwd(q, k, v, o_in, lse_ref, do, 500, 400, True, scale)
+    check_close("dQacc", f64(acc), g[0] + 0.5, TOL[dtype]["grad"])
+    check_close("dK", f64(dk), g[1], TOL[dtype]["grad"], True)
+    check_close("dV", f64(dv), g[2], TOL[dtype]["grad"], True)
+
+
 @pytest.mark.parametrize("hq,hkv", [(16, 16), (16, 4), (24, 8)])
 def test_several_heads_per_xcd(gpu, hq, hkv):
     """Head counts that are multiples of 8: each of the 8 XCDs owns hq/8 query heads (hkv/8 KV

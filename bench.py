@@ -39,11 +39,18 @@ KERNEL_SOURCES = {"fwd": ["fwd_bf16.hip", "common.hpp"],
 
 
 def kernel_source_hash(kernel):
+    """sha256 of the kernel's source files with comments and blank lines removed, so that a
+    counter record outlives edits of the comments alone."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(REPO, "paper_2502_21231_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(REPO, "paper_2502_21231_amd", "csrc", f), encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        code = "\n".join(line.rstrip() for line in text.splitlines() if line.strip())
+        h.update(code.encode("utf-8"))
     return h.hexdigest()
 
 

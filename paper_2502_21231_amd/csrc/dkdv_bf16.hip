@@ -25,10 +25,11 @@
 //   are walked from the diagonal (MASKED tiles first) to the end of the segment.
 //   With a group of several, from the last tile of the segment down to the
 //   diagonal, the heads of the group innermost: the workgroups of one segment's
-//   key tiles that run together on an XCD (one KV head per XCD) then read the same
+//   key tiles for one KV head that run together on an XCD then read the same
 //   query tile of the same head at about the same time, once from HBM into that
 //   XCD's L2; walked upwards, each starts at its own diagonal, and its head
-//   changes at its own time.
+//   changes at its own time.  Which key tile and KV head a workgroup takes, and
+//   how the XCDs share them, is block_work's (common.hpp).
 //   Query rows past the segment use LSE = +inf (P = 0), rows whose LSE is
 //   -inf (no visible key) also get P = 0.
 //

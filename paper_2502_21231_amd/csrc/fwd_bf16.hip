@@ -1,7 +1,8 @@
 // bf16 attention forward for gfx950: tiled online softmax on MFMA.
 //
 // One workgroup = one query tile of the work list (kFwdBM = 128 rows) for one
-// query head; 4 waves, each owning 32 query rows.  The key loop walks the
+// query head (which ones, and how the XCDs share them: block_work in common.hpp);
+// 4 waves, each owning 32 query rows.  The key loop walks the
 // tile's visible key tiles (kFwdBN = 64 keys): the FULL ones first without any
 // score mask, then the MASKED ones (causal diagonal / ragged key tail).
 //

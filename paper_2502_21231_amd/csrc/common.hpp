@@ -51,21 +51,23 @@ struct WsHeader {
   int32_t pad[62];
 };
 
-// A segment streams this many rows (b_len) or more: its run is walked one head at a time.
-constexpr int kHeadMajorRows = 16384;
+// The dK/dV kernel walks a segment one head at a time from this many streamed rows (b_len)
+// on; the forward and dQ kernels do so for every segment.
+constexpr int kHeadMajorRowsDkdv = 16384;
 
 // Work item and head of this workgroup in a grid of n_items * n_heads blocks; false when it
 // has none.  Blocks are dealt to the 8 XCDs round-robin (block b runs on XCD b % 8), so with
 // n_heads a multiple of 8 each XCD owns the hx = n_heads / 8 heads x*hx .. x*hx+hx-1 and walks
 // the list segment by segment.  Inside a segment's run its heads are interleaved item by
-// item, except where the segment streams at least kHeadMajorRows rows and the XCD's heads
-// read more than one stream (hx > heads_per_stream: heads that share a KV head share its
-// K/V stream): there the XCD walks one head's items at a time, so that the workgroups
-// resident on it read one stream, not hx / heads_per_stream, and each tile of it comes into
-// the XCD's L2 that many times less often.
+// item, except where the segment streams at least min_rows rows and the XCD's heads read
+// more than one stream (hx > heads_per_stream: heads that share a KV head share its K/V
+// stream): there the XCD walks one head's items at a time, so that the workgroups resident
+// on it read one stream, not hx / heads_per_stream, and each tile of it comes into the
+// XCD's L2 that many times less often.
 __device__ __forceinline__ bool block_work(const WsHeader* __restrict__ hdr,
                                            const WorkItem* __restrict__ items, int n_heads,
-                                           int heads_per_stream, WorkItem& it, int& head) {
+                                           int heads_per_stream, int min_rows, WorkItem& it,
+                                           int& head) {
   const int b = blockIdx.x;
   const int n_items = hdr->n_items;
   if ((n_heads & 7) != 0) {
@@ -81,7 +83,7 @@ __device__ __forceinline__ bool block_work(const WsHeader* __restrict__ hdr,
   const WorkItem gi = items[g];
   const int r = jb - gi.run0 * hx;  // 0 <= r < nrun * hx: this block's place in the run
   int i, hl;
-  if (hx > heads_per_stream && gi.b_len >= kHeadMajorRows) {
+  if (hx > heads_per_stream && gi.b_len >= min_rows) {
     hl = r / gi.nrun;
     i = gi.run0 + (r - hl * gi.nrun);
   } else {

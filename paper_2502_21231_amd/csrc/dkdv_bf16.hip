@@ -68,7 +68,7 @@ void dkdv_bf16_kernel(const BwdParams p) {
 
   WorkItem it;
   int hk;  // KV head; each reads the Q/dO stream of its own query heads
-  if (!block_work(p.hdr, p.items, p.hkv, 1, it, hk)) return;
+  if (!block_work(p.hdr, p.items, p.hkv, 1, kHeadMajorRowsDkdv, it, hk)) return;
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, c = lane & 31, hh = lane >> 5;

@@ -39,7 +39,7 @@ void dq_bf16_kernel(const BwdParams p) {
 
   WorkItem it;
   int h;  // query head; the query heads of one KV group share its K/V stream
-  if (!block_work(p.hdr, p.items, p.hq, p.group, it, h)) return;
+  if (!block_work(p.hdr, p.items, p.hq, p.group, 0, it, h)) return;
   const int hk = h / p.group;
 
   const int tid = threadIdx.x;

@@ -50,3 +50,24 @@ def test_more_than_one_gpu_is_refused_before_any_device_work():
     assert r.returncode == 2, (r.returncode, r.stderr[-500:])
     assert "--gpus 2 is not supported" in r.stderr
     assert r.stdout.strip() == ""
+
+
+def test_counter_records_survive_comment_edits_only(tmp_path, monkeypatch):
+    """A counter record is matched to the kernel's sources without their comments and blank
+    lines: editing a comment keeps it, editing code drops it."""
+    import shutil
+    csrc = os.path.join(ROOT, "paper_2502_21231_amd", "csrc")
+    dst = tmp_path / "paper_2502_21231_amd" / "csrc"
+    dst.mkdir(parents=True)
+    for f in set(sum(bench.KERNEL_SOURCES.values(), [])):
+        shutil.copy(os.path.join(csrc, f), dst / f)
+    monkeypatch.setattr(bench, "REPO", str(tmp_path))
+    before = {k: bench.kernel_source_hash(k) for k in bench.KERNEL_SOURCES}
+    p = dst / "dkdv_bf16.hip"
+    text = p.read_text()
+    p.write_text("// a new first line\n\n" + text.replace("\n", "\n\n", 3) + "/* and a block\n comment */\n")
+    assert {k: bench.kernel_source_hash(k) for k in bench.KERNEL_SOURCES} == before
+    p.write_text(text.replace("n_vis - 1 - s", "n_vis - s", 1))
+    after = {k: bench.kernel_source_hash(k) for k in bench.KERNEL_SOURCES}
+    assert after["bwd_dkdv"] != before["bwd_dkdv"]
+    assert after["fwd"] == before["fwd"] and after["bwd_dq"] == before["bwd_dq"]

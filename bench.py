@@ -32,9 +32,9 @@ if ROOT not in sys.path:
 BF16_PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12   # 2516.6: MI355X dense bf16 MFMA (AMD's 2.5 PF)
 REPO = os.path.dirname(os.path.abspath(__file__))
 # sources whose text fixes each timed kernel (a counter record applies only to them)
-KERNEL_SOURCES = {"fwd": ["fwd_bf16.hip", "common.hpp"],
-                  "bwd_dq": ["dq_bf16.hip", "bwd_common.hpp", "common.hpp"],
-                  "bwd_dkdv": ["dkdv_bf16.hip", "bwd_common.hpp", "common.hpp"],
+KERNEL_SOURCES = {"fwd": ["fwd_bf16.hip", "attn.hpp", "common.hpp"],
+                  "bwd_dq": ["dq_bf16.hip", "bwd_common.hpp", "attn.hpp", "common.hpp"],
+                  "bwd_dkdv": ["dkdv_bf16.hip", "bwd_common.hpp", "attn.hpp", "common.hpp"],
                   "xent": ["xent.hip", "common.hpp"]}
 
 

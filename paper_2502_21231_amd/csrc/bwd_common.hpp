@@ -3,7 +3,7 @@
 // dK/dV kernel key tiles.
 #pragma once
 
-#include "common.hpp"
+#include "attn.hpp"
 
 namespace bs {
 

@@ -9,7 +9,7 @@
 #include <mutex>
 #include <vector>
 
-#include "common.hpp"
+#include "attn.hpp"
 
 // Scratch of the allocation-free forward (bs_attn_varlen_fwd_noalloc): the plan that the
 // forward kernel walks (header, per-segment offsets, work list).  Each device holds its own
@@ -129,10 +129,10 @@ bool valid_op(int op) { return op >= BS_OP_VARLEN_FWD && op <= BS_OP_PACKED_CHUN
 // Plans an op runs, in launch order: the forward walks query tiles; the
 // backward plans twice, query tiles for its dQ kernel, then key tiles for its
 // dK/dV kernel.
-int plans_of(int op, int dtype, PlanCfg out[2]) {
-  if (dtype == BS_BF16) {
+int plans_of(int op, const bs_dims& d, PlanCfg out[2]) {
+  if (d.dtype == BS_BF16) {
     out[0] = PlanCfg{kPlanFwd, kFwdBM, kFwdBN};
-    out[1] = PlanCfg{kPlanBwd, kBwdBN, kBwdBM};
+    out[1] = PlanCfg{kPlanBwd, kBwdBN, bwd_bm(d.head_dim)};
   } else {
     out[0] = PlanCfg{kPlanFwd, kF32BM, kF32BN};
     out[1] = PlanCfg{kPlanBwd, kF32BN, kF32BM};
@@ -180,7 +180,7 @@ int check_scale(float s) {
 WsLayout layout_of(int op, const bs_dims& d, int64_t nseg) {
   WsLayout L = {};
   PlanCfg cfg[2];
-  const int np = plans_of(op, d.dtype, cfg);
+  const int np = plans_of(op, d, cfg);
   const bool varlen = is_varlen(op);
   int64_t mi = 0;
   for (int i = 0; i < np; ++i) {
@@ -223,7 +223,7 @@ hipError_t run_plan(int op, const bs_dims& d, int i, const int32_t* cu_q, const 
                     int32_t max_seqlen, int64_t q_off, int64_t k_off, int causal, void* ws,
                     const WsLayout& L, WsLayout* Lp, hipStream_t s) {
   PlanCfg cfg[2];
-  plans_of(op, d.dtype, cfg);
+  plans_of(op, d, cfg);
   const bool varlen = is_varlen(op);
   *Lp = L;
   Lp->max_items = max_items_of(cfg[i], d, varlen ? num_seqs : 1, varlen);
@@ -639,7 +639,7 @@ int bs_attn_plan_export(int op, const bs_dims* dims, const int32_t* cu_seqlens_q
   hipStream_t s = static_cast<hipStream_t>(stream);
   // the plan the op's main kernel walks: the last one of the op
   PlanCfg cfg[2];
-  const int np = plans_of(op, dims->dtype, cfg);
+  const int np = plans_of(op, *dims, cfg);
   WsLayout Lp;
   BS_HIP(run_plan(op, *dims, np - 1, cu_seqlens_q, cu_seqlens_k, q_pos, k_pos, num_seqs,
                   max_seqlen, q_pos_offset, k_pos_offset, causal, workspace, L, &Lp, s),

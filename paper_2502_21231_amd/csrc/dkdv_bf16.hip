@@ -2,10 +2,11 @@
 // atomics).
 //
 // dkdv_bf16_kernel (key-major, walks the backward work list: 128-key tiles
-//   over 64-row query tiles).  8 waves, 2 per SIMD, in pairs: both waves of
+//   over query tiles of 96 rows at head_dim 128, 64 at head_dim 64).  8 waves,
+//   2 per SIMD, in pairs: both waves of
 //   pair b own the 32-key block b of the tile, and split the work by role.
 //     S wave  (holds K of its keys): S = Q K^T, P = exp2(S*c - LSE*log2e)
-//                                    (lane = one key, 64 query rows), hands the
+//                                    (lane = one key, the tile's query rows), hands the
 //                                    bf16 P that feeds its own products to its
 //                                    partner through LDS, and accumulates
 //                                    dV^T += dO^T P.
@@ -29,7 +30,7 @@
 //   query tile of the same head at about the same time, once from HBM into that
 //   XCD's L2; walked upwards, each starts at its own diagonal, and its head
 //   changes at its own time.  Which key tile and KV head a workgroup takes, and
-//   how the XCDs share them, is block_work's (common.hpp).
+//   how the XCDs share them, is block_work's (attn.hpp).
 //   Query rows past the segment use LSE = +inf (P = 0), rows whose LSE is
 //   -inf (no visible key) also get P = 0.
 //
@@ -48,13 +49,13 @@ namespace {
 template <int D, bool kGroupOrder>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void dkdv_bf16_kernel(const BwdParams p) {
-  constexpr int BM = kBwdBM, BN = kBwdBN;
+  constexpr int BM = bwd_bm(D), BN = kBwdBN;
   constexpr int KK = D / 16, DB = D / 32;
   constexpr int MB = BM / 32;                 // 32-row blocks of a query tile
   constexpr int QS = BM / 16;                 // 16-row contraction steps of a query tile
   constexpr int QTILE = BM * D;               // swizzled [BM][D] query tile
   constexpr int NW = 8;
-  static_assert(BM == 64 && BN == 128, "tile shape");
+  static_assert((BM == 64 || BM == 96) && BN == 128, "tile shape");
   // Q and dO tiles, double-buffered; each buffer is its own array (Q tile, then
   // dO tile), so that the compiler can tell the copy into one from the reads of
   // the other
@@ -129,7 +130,7 @@ void dkdv_bf16_kernel(const BwdParams p) {
     dma_tile<D, BM, NW>(QDd, p.q + qo, (int)qstride, last, w, lane);
     dma_tile<D, BM, NW>(QDd + QTILE, p.dout + qo, (int)qstride, last, w, lane);
     {
-      const int r = ct & (BM - 1);
+      const int r = ct % BM;
       row_ok = r <= last;
       const int64_t li = (int64_t)h * p.total_q + q_glob0 + (row_ok ? r : 0);
       row_r = (ct < BM ? p.lse : p.dvec)[li];
@@ -151,6 +152,8 @@ void dkdv_bf16_kernel(const BwdParams p) {
   // phase 1 reads rows of Q (role 0) or dO (role 1); phase 2 reads dO (role 0)
   // or Q (role 1) transposed
   const int base1 = role * QTILE, base2 = (1 - role) * QTILE;
+  // lane bases of the row reads and the transposing reads (the XOR form of the swizzle)
+  const int rbase = swz_row_base<D>(lane), tbase = swz_tr_base<D>(lane);
   bf16x8* pslot = Ps + kb * QS * 64 + lane;
 
   // one query tile: consume (QDb, Rb) while tile i+1 is copied into (QDn, Rn),
@@ -178,7 +181,7 @@ void dkdv_bf16_kernel(const BwdParams p) {
     for (int kk = 0; kk < KK; ++kk) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&A1[swz_off<D>(mb * 32 + c, kk * 2 + hh)]);
+        const bf16x8 a = lds_row16(A1, (rbase ^ (kk << 5)) + mb * 64 * D);
         s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, frag[kk], s[mb], 0, 0, 0);
       }
     }
@@ -253,8 +256,8 @@ void dkdv_bf16_kernel(const BwdParams p) {
     for (int qs = 0; qs < QS; ++qs) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const bf16x8 a = lds_read_tr2(A2 + swz_tr_off<D>(qs * 16, db * 32, 0, lane),
-                                      A2 + swz_tr_off<D>(qs * 16, db * 32, 1, lane));
+        const bf16x8 a = lds_tr16(A2, (tbase ^ (db << 6)) + qs * 32 * D,
+                                  (tbase ^ ((db << 6) | 32)) + qs * 32 * D + 16 * D);
         acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ob[qs], acc[db], 0, 0, 0);
       }
     }

@@ -6,7 +6,7 @@
 // with the shared key (or query) tile staged in LDS.  Exact-order fp32 dot
 // products, no MFMA: they exist so that float32 inputs are answered with
 // float32 accuracy.
-#include "common.hpp"
+#include "attn.hpp"
 
 namespace bs {
 namespace {

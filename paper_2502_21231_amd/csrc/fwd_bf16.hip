@@ -1,7 +1,7 @@
 // bf16 attention forward for gfx950: tiled online softmax on MFMA.
 //
 // One workgroup = one query tile of the work list (kFwdBM = 128 rows) for one
-// query head (which ones, and how the XCDs share them: block_work in common.hpp);
+// query head (which ones, and how the XCDs share them: block_work in attn.hpp);
 // 4 waves, each owning 32 query rows.  The key loop walks the
 // tile's visible key tiles (kFwdBN = 64 keys): the FULL ones first without any
 // score mask, then the MASKED ones (causal diagonal / ragged key tail).
@@ -34,7 +34,7 @@
 // is skipped on almost every tile; p then stays below 2^8, which neither the
 // bf16 P nor the fp32 sums mind, and O = acc / l, LSE = (m + log2 l) ln 2 use
 // the same m.
-#include "common.hpp"
+#include "attn.hpp"
 
 namespace bs {
 namespace {

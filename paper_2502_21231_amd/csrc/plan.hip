@@ -22,7 +22,7 @@
 //   plan_rank  : one thread per segment: its first slot in the ordered list
 //   plan_emit  : one thread per list entry, fills its fields at its slot
 // or, for up to 1024 segments, the same three steps in one workgroup (plan_fused).
-#include "common.hpp"
+#include "attn.hpp"
 
 namespace bs {
 namespace {

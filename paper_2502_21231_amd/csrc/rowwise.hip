@@ -3,7 +3,7 @@
 // Each (token, head) row of head_dim elements is handled by a group of
 // head_dim/8 (bf16) or head_dim/4 (fp32) lanes, one 16-byte vector per lane,
 // so every row is read and written with fully coalesced 16-byte accesses.
-#include "common.hpp"
+#include "attn.hpp"
 
 namespace bs {
 namespace {
